@@ -1,0 +1,230 @@
+"""The HiFA4 (C4V16) causal prefill forward, step by step.
+
+Paper: Algorithm 1 (C4V16-Aux), without the Q-Mean steps; Background,
+"FlashAttention tiling" (online softmax); Section 4.5 (P-Reordering,
+Theorem 1, fused normalizer [V|1]); "P-Reordering under online softmax";
+Appendix C (quantized tensors, FP16 operations, GQA).
+
+Readings fixed here (the paper is silent on them):
+  * logical KV block = 64 keys = one P group, processed in ascending order;
+    blocks are aligned to each sequence's first token;
+  * Q~ and K~ are HIF4-quantized along the head dimension (64-channel groups),
+    V along tokens (64 tokens of one channel; a partial last group is zero
+    padded), P along the 64 keys of a block -- every group lies along the
+    contraction axis of its GEMM;
+  * scores: per 64-channel group g the dot t_g of the dequantized operands is
+    exact; S_acc = (((t_0 + t_1) + t_2) + ...) with fp32 round-to-nearest
+    additions; S2 = fp16(fp32(S_acc * c)) with c = fp32(log2(e)/sqrt(D)), so
+    the softmax runs in base 2 (2^(S2-m) equals exp(S/sqrt(D) - m') exactly in
+    real arithmetic);
+  * running max m and the weights are fp16: m_new = max(m, rowmax S2),
+    x = fp16(S2 - m_new), P16 = E(x), r = E(fp16(m - m_new));
+  * P-Reordering: P^ = HIF4(P16 over the block), O <- r*O + P^ V^,
+    l <- r*l + rowsum(P^); the inconsistent (Direct) variant keeps
+    l <- r*l + rowsum(P16) (Theorem 1's partition sum Z);
+  * O and l are accumulated in float64 here (fp32 on the GPU; the paper keeps
+    l in FP16, which cannot hold sums past 2048 -- a documented deviation);
+  * finalize: O = fp16(fp32(O / l)); LSE = m*ln2 + ln(l) (natural log, fp32).
+  * causal: key j is visible to query i (same sequence) iff j <= i.
+
+``arith="exact"`` runs the same loop with no quantization and no fp16
+rounding (float64 scores, exp and state), for the brute-force pin.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+from . import hif4
+from .smooth import apply as smooth_apply
+from .softmax16 import exp2_fp16, sub_fp16
+
+BLOCK = 64
+LN2 = math.log(2.0)
+
+
+def score_scale(head_dim: int) -> np.float32:
+    """c = fp32(log2(e) / sqrt(D)), computed in float64 and rounded once."""
+    return np.float32(math.log2(math.e) / math.sqrt(head_dim))
+
+
+def quantize_rows(x):
+    """HIF4 along the last axis (groups of 64 consecutive channels)."""
+    lead, d = x.shape[:-1], x.shape[-1]
+    f = hif4.quantize(np.asarray(x, np.float64).reshape(*lead, d // 64, 64))
+    return f
+
+
+def quantize_tokens(v):
+    """HIF4 of V along tokens: v [L, D] -> groups of 64 tokens per channel,
+    zero padded to a multiple of 64.  Returns (fields over [D, L/64, 64],
+    vhat [Lpad, D])."""
+    L, d = v.shape
+    lp = -(-L // BLOCK) * BLOCK
+    vp = np.zeros((lp, d), np.float64)
+    vp[:L] = v.astype(np.float64)
+    g = vp.T.reshape(d, lp // BLOCK, BLOCK)
+    f = hif4.quantize(g)
+    vhat = f["xhat"].reshape(d, lp).T.copy()
+    return f, vhat
+
+
+def scores_hif4(qhat, khat, head_dim):
+    """S2 = fp16(fp32(S_acc * c)) from dequantized operands (float64 [n, D]
+    and [L, D]).  Each group dot is exact in float64 (integer grid, at most
+    22 significant bits) and in fp32; the fp32 partial sums round to nearest."""
+    c = score_scale(head_dim)
+    s_acc = None
+    for g in range(head_dim // 64):
+        sl = slice(64 * g, 64 * g + 64)
+        t = (qhat[:, sl] @ khat[:, sl].T).astype(np.float32)   # exact
+        s_acc = t if s_acc is None else (s_acc + t)             # fp32 RN add
+    return (s_acc * c).astype(np.float16)
+
+
+def scores_fp16(q, k, head_dim):
+    """FP16-operand variant: fp32 dot of the fp16 operands, times c, to fp16."""
+    c = score_scale(head_dim)
+    s = (q.astype(np.float64) @ k.astype(np.float64).T).astype(np.float32)
+    return (s * c).astype(np.float16)
+
+
+def online_softmax(s2, vop, rows, length, quantize_p, want_p=False, arith="contract"):
+    """Algorithm 1's tile loop for the query rows ``rows`` of one (sequence,
+    head).  s2: [n, length] scores of those rows (fp16, or float64 when
+    arith == "exact"); vop: [Lpad, D] value operand (V^ or V) in float64."""
+    n, d = len(rows), vop.shape[1]
+    nblk = -(-length // BLOCK)
+    exact = arith == "exact"
+    m = np.full(n, -np.inf, np.float64 if exact else np.float16)
+    o = np.zeros((n, d))
+    l_con = np.zeros(n)
+    l_mis = np.zeros(n)
+    p_codes = np.zeros((n, nblk, 32), np.uint8) if want_p else None
+    p_meta = np.zeros((n, nblk), np.uint32) if want_p else None
+    eps_blk = np.full((n, nblk), np.nan) if want_p else None
+    for jb in range(nblk):
+        act = np.nonzero(rows >= BLOCK * jb)[0]
+        if act.size == 0:
+            continue
+        keys = np.arange(BLOCK * jb, BLOCK * jb + BLOCK)
+        blk = np.full((act.size, BLOCK), -np.inf, s2.dtype)
+        nk = min(BLOCK, length - BLOCK * jb)
+        blk[:, :nk] = s2[act, BLOCK * jb:BLOCK * jb + nk]
+        blk = np.where(keys[None, :] <= rows[act, None], blk, -np.inf).astype(s2.dtype)
+        m_new = np.maximum(m[act], blk.max(axis=1))                 # running max
+        if exact:
+            p = np.exp2(blk - m_new[:, None])
+            r = np.exp2(m[act] - m_new)
+        else:
+            p = exp2_fp16(sub_fp16(blk, m_new[:, None]))            # P16
+            r = exp2_fp16(sub_fp16(m[act], m_new)).astype(np.float64)
+        p64 = p.astype(np.float64)
+        if quantize_p:
+            f = hif4.quantize(p64)                                   # P-Reordering
+            phat = f["xhat"]
+            if want_p:
+                c_, m_ = hif4.pack(f)
+                p_codes[act, jb] = c_
+                p_meta[act, jb] = m_
+        else:
+            phat = p64
+        if want_p:
+            with np.errstate(invalid="ignore", divide="ignore"):
+                eps_blk[act, jb] = phat.sum(1) / p64.sum(1) - 1.0
+        o[act] = o[act] * r[:, None] + phat @ vop[BLOCK * jb:BLOCK * jb + BLOCK]
+        l_con[act] = l_con[act] * r + phat.sum(axis=1)                # fused [V|1]
+        l_mis[act] = l_mis[act] * r + p64.sum(axis=1)                 # Direct: Z
+        m[act] = m_new
+    return {"o_num": o, "l_con": l_con, "l_mis": l_mis, "m": m.astype(np.float64),
+            "p_codes": p_codes, "p_meta": p_meta, "eps_blk": eps_blk}
+
+
+def _as_varlen(q, k, v, cu_seqlens):
+    if cu_seqlens is None:
+        b, s = q.shape[:2]
+        return (q.reshape(b * s, *q.shape[2:]), k.reshape(b * s, *k.shape[2:]),
+                v.reshape(b * s, *v.shape[2:]), np.arange(b + 1, dtype=np.int64) * s)
+    return q, k, v, np.asarray(cu_seqlens, np.int64)
+
+
+def attention_fwd(q, k, v, s=None, cu_seqlens=None, norm="preorder", operands="hif4",
+                  heads=None, seqs=None, rows=None, want_p=False, arith="contract"):
+    """HiFA4 forward on fp16 inputs.
+
+    q [B,S,Hq,D] (or [T,Hq,D] with cu_seqlens), k/v [.., Hkv, D], s fp32
+    [Hkv, D] or None (no smoothing).  ``heads``/``seqs``/``rows`` restrict the
+    computation to a sample (rows are positions within each sequence).
+    Returns a dict keyed by (seq, head) with o (float64 O/l), o16, lse, and,
+    with want_p, the canonical P^ codes/metadata per (row, block)."""
+    qv, kv, vv, cu = _as_varlen(q, k, v, cu_seqlens)
+    hq, hkv, d = qv.shape[1], kv.shape[1], qv.shape[2]
+    grp = hq // hkv
+    if operands == "hif4" and s is not None:
+        qv, kv = smooth_apply(qv, kv, s, hkv)
+    out = {}
+    for b in (range(len(cu) - 1) if seqs is None else seqs):
+        t0, t1 = int(cu[b]), int(cu[b + 1])
+        length = t1 - t0
+        rr = np.arange(length) if rows is None else np.asarray([r for r in rows if r < length])
+        vcache = {}
+        for h in (range(hq) if heads is None else heads):
+            hk = h // grp
+            qs, ks, vs = qv[t0:t1, h], kv[t0:t1, hk], vv[t0:t1, hk]
+            if arith == "exact":
+                s2 = (qs.astype(np.float64)[rr] @ ks.astype(np.float64).T) * (math.log2(math.e) / math.sqrt(d))
+                vop = np.zeros((-(-length // BLOCK) * BLOCK, d)); vop[:length] = vs
+                res = online_softmax(s2, vop, rr, length, False, arith="exact")
+            elif operands == "hif4":
+                qhat = quantize_rows(qs[rr])["xhat"].reshape(len(rr), d)
+                khat = quantize_rows(ks)["xhat"].reshape(length, d)
+                if hk not in vcache:
+                    vcache[hk] = quantize_tokens(vs)[1]
+                s2 = scores_hif4(qhat, khat, d)
+                res = online_softmax(s2, vcache[hk], rr, length, True, want_p=want_p)
+            else:
+                s2 = scores_fp16(qs[rr], ks, d)
+                vop = np.zeros((-(-length // BLOCK) * BLOCK, d)); vop[:length] = vs
+                res = online_softmax(s2, vop, rr, length, False, want_p=want_p)
+            lsum = res["l_mis"] if norm == "inconsistent" else res["l_con"]
+            o = res["o_num"] / lsum[:, None]
+            res["o"] = o
+            res["o16"] = o.astype(np.float32).astype(np.float16)
+            res["lse"] = (res["m"] * LN2 + np.log(lsum)).astype(np.float32)
+            res["rows"] = rr
+            out[(b, h)] = res
+    return out
+
+
+def quantize_qk(q, k, s=None):
+    """Smooth-QK then HIF4 of Q~ and K~ along D, in the canonical packed
+    layout: codes [..., H, D/64, 32] uint8, meta [..., H, D/64] uint32."""
+    hkv = k.shape[-2]
+    if s is not None:
+        q, k = smooth_apply(q, k, s, hkv)
+    qc, qm = hif4.pack(quantize_rows(q))
+    kc, km = hif4.pack(quantize_rows(k))
+    return qc, qm, kc, km
+
+
+def quantize_v(v, cu_seqlens=None):
+    """HIF4 of V along tokens, canonical layout per (sequence, kv head,
+    channel, 64-token group): codes [G, Hkv, D, 32], meta [G, Hkv, D] where G
+    enumerates the token groups of all sequences in order."""
+    if cu_seqlens is None:
+        b, s = v.shape[:2]
+        v = v.reshape(b * s, *v.shape[2:])
+        cu = np.arange(b + 1) * s
+    else:
+        cu = np.asarray(cu_seqlens)
+    hkv, d = v.shape[1], v.shape[2]
+    codes, metas = [], []
+    for b in range(len(cu) - 1):
+        for_h_c, for_h_m = [], []
+        for h in range(hkv):
+            f, _ = quantize_tokens(v[cu[b]:cu[b + 1], h])       # [D, G_b, 64]
+            c_, m_ = hif4.pack(f)
+            for_h_c.append(c_.transpose(1, 0, 2)); for_h_m.append(m_.T)
+        codes.append(np.stack(for_h_c, axis=1)); metas.append(np.stack(for_h_m, axis=1))
+    return np.concatenate(codes), np.concatenate(metas)
