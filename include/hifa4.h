@@ -1,0 +1,214 @@
+/*
+ * hifa4.h -- C ABI of libhifa4: the HiFA4 causal prefill attention forward on
+ * AMD Instinct MI355X (gfx950).
+ *
+ * HiFA4 (arXiv 2607.04302) runs both FlashAttention contractions, QK^T and PV,
+ * on 4-bit HIF4 operands while the online-softmax state stays in FP16
+ * (Section 3, "C4V16"), with two corrections:
+ *   - Smooth-QK (Eq. 1, Sections 4.2-4.4): a calibration-static per-channel
+ *     rescale q*s, k/s applied after RoPE, fused into the quantization;
+ *   - P-Reordering (Section 4.5, Theorem 1): P is quantized first and the
+ *     softmax normalizer is accumulated from that same P^ inside the PV
+ *     contraction, through an appended ones block [V^ | 1].
+ * Algorithm 1 gives the loop; the Q-Mean auxiliary of its lines for mu is not
+ * part of this library.
+ *
+ * Conventions (all entry points):
+ *   - Tensor pointers are DEVICE pointers owned by the caller; the library
+ *     never allocates, frees or retains device memory, and keeps no device
+ *     state between calls.  Where a host pointer is meant, it says so.
+ *   - Fixed-length problems use BSHD layout ([batch, seqlen, heads, dim],
+ *     row-major, contiguous).  Variable-length problems pass cu_seqlens and
+ *     use THD layout ([total_tokens, heads, dim]).
+ *   - fp16 means IEEE binary16, fp32 IEEE binary32.
+ *   - Work is enqueued on `stream` (a hipStream_t passed as void*; NULL is the
+ *     default stream) and is asynchronous unless stated.  Arguments are
+ *     validated synchronously; a launch failure maps to HIFA4_ERR_HIP.
+ *     Device faults surface at the caller's next synchronization.
+ *   - Nothing throws across the ABI.  On a non-OK status, hifa4_last_error()
+ *     returns a message for the calling thread.
+ *   - Inputs must be finite and keep |S * log2(e)/sqrt(D)| within the fp16
+ *     range (the paper's FP16 softmax state); other inputs are outside the
+ *     contract.
+ *
+ * HIF4 group format (the library's reading; see the HIF4 paragraph of the
+ * paper's Background section): 64 elements along the contraction axis of the
+ * GEMM that consumes them; an unsigned E6M2 base b (bias 31, byte = e<<2|m,
+ * value (1+m/4)*2^(e-31)), the smallest with 1.75*b >= max|x|; level-2 bit j
+ * (8 elements) set iff that block's max <= 0.875*b; level-3 bit q (4
+ * elements) set iff its max <= 0.875*b*2^-E2[q/2]; a set bit halves the scale;
+ * element code u = floor(|x|/step + 1/2) with step = b*2^-(E2+E3)/4, u in 0..7,
+ * sign-magnitude nibble sign<<3|u (zero stored as +0).
+ *
+ * Canonical packed layout, per group: 32 code bytes (element 2i in the low
+ * nibble of byte i, element 2i+1 in the high nibble) and one little-endian
+ * uint32 of metadata: base | E2 bits << 8 | E3 bits << 16 (bit j = block j).
+ * 36 bytes per 64 values = 4.5 bits per value.
+ */
+#ifndef HIFA4_H
+#define HIFA4_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  HIFA4_OK = 0,
+  HIFA4_ERR_INVALID_ARGUMENT = -1, /* null pointer, bad size or shape        */
+  HIFA4_ERR_UNSUPPORTED = -2,      /* valid but not implemented (see below)  */
+  HIFA4_ERR_WORKSPACE = -3,        /* workspace too small                    */
+  HIFA4_ERR_HIP = -4               /* a HIP runtime call or launch failed    */
+} hifa4_status;
+
+/* Shape of one causal prefill problem.  Q has num_heads_q heads, K and V have
+ * num_heads_kv; query head h reads key/value head h / (num_heads_q /
+ * num_heads_kv) (GQA, Appendix C).  Queries and keys of a sequence have equal
+ * lengths and key j is visible to query i iff j <= i.
+ *   head_dim     in {64, 128, 256};
+ *   max_seqlen   fixed length (BSHD) or, with cu_seqlens, an upper bound of
+ *                every sequence length (host value);
+ *   cu_seqlens   NULL for BSHD, else a DEVICE int32 array [batch+1] of
+ *                non-decreasing prefix sums starting at 0 (THD layout);
+ *   total_tokens with cu_seqlens: cu_seqlens[batch] (host value); ignored
+ *                for BSHD (batch*max_seqlen);
+ *   causal       must be 1. */
+typedef struct {
+  int32_t batch;
+  int32_t num_heads_q;
+  int32_t num_heads_kv;
+  int32_t head_dim;
+  int32_t max_seqlen;
+  const int32_t* cu_seqlens;
+  int32_t total_tokens;
+  int32_t causal;
+} hifa4_problem;
+
+typedef enum {
+  HIFA4_NORM_PREORDER = 0,     /* P-Reordering: l accumulates P^ (Section 4.5) */
+  HIFA4_NORM_INCONSISTENT = 1  /* Direct baseline: l accumulates pre-quantization
+                                  P while PV uses P^ (Theorem 1, "mismatched") */
+} hifa4_norm;
+
+typedef enum {
+  HIFA4_OPERANDS_HIF4 = 0,  /* both contractions on HIF4 operands (C4V16)     */
+  HIFA4_OPERANDS_FP16 = 1   /* same loop on fp16 operands, no quantization and
+                               no smoothing: the FP16 reference (C16V16) */
+} hifa4_operands;
+
+/* Options of hifa4_attention_fwd.
+ *   smooth_qk      0: the scale vector is ignored (treated as all ones);
+ *   debug_p_codes  NULL, or a DEVICE uint8 buffer [num_heads_q, T, NB, 32]
+ *                  receiving the canonical codes of every P^ group, where T
+ *                  is the token count (BSHD: batch*max_seqlen) and
+ *                  NB = ceil(max_seqlen/64); entry (h, t, J) is written for
+ *                  the 64-key blocks J <= i/64 that query t (position i in
+ *                  its sequence) sees, other entries are left untouched;
+ *   debug_p_meta   NULL, or a DEVICE uint32 buffer [num_heads_q, T, NB] with
+ *                  the matching metadata words.  Both or neither.
+ * Debug dumps are only produced for HIFA4_OPERANDS_HIF4. */
+typedef struct {
+  int32_t norm;       /* hifa4_norm      */
+  int32_t operands;   /* hifa4_operands  */
+  int32_t smooth_qk;
+  void* debug_p_codes;
+  void* debug_p_meta;
+} hifa4_fwd_options;
+
+/* Host-side calibration report (Table 1 statistics and the gate decision). */
+typedef struct {
+  double rho_k;        /* max|K| / P99(|K|) over all calibration K elements */
+  double t_kq;         /* max|K| / max|Q|                                     */
+  int32_t branch;      /* 0 bypass, 1 mild, 2 strong                          */
+  float alpha_used;
+} hifa4_calib_report;
+
+/* Bytes of device workspace hifa4_attention_fwd needs for this problem and
+ * options (0 on invalid arguments).  The workspace holds the MFMA-ready K and
+ * V operands written by the pre-pass. */
+size_t hifa4_workspace_bytes(const hifa4_problem* p, const hifa4_fwd_options* opt);
+
+/* Bytes of device workspace hifa4_calibrate_smooth_qk needs. */
+size_t hifa4_calibrate_workspace_bytes(const hifa4_problem* p, int32_t n_calib);
+
+/* Offline Smooth-QK calibration (Eq. 1; Sections 4.3-4.4; Appendix C).
+ * q_calib: DEVICE fp16 [n_calib, max_seqlen, num_heads_q, head_dim];
+ * k_calib: DEVICE fp16 [n_calib, max_seqlen, num_heads_kv, head_dim]
+ * (n_calib fixed-length sequences stacked on the leading axis; p->batch and
+ * p->cu_seqlens are ignored).  Per sequence, the GPU reduces max|K| over
+ * tokens and max|Q| over tokens and the query heads of each group, per (kv
+ * head, channel), and a 32768-bin histogram of |K| (exact for fp16).  On the
+ * host, in float64: the RMS over sequences, s = Kbar^alpha / Qbar^(1-alpha)
+ * rounded once to fp32 (s = 1 where a statistic is 0 or s is not finite),
+ * and the gate statistics rho_K = max|K| / P99|K| (linear interpolation
+ * between order statistics) and T = max|K| / max|Q|.
+ *   alpha > 0  use this alpha;  alpha == 0  bypass (s = 1);
+ *   alpha < 0  the gate picks: strong (0.5) if rho_K >= 6 and T > 3,
+ *              mild (0.25) if rho_K >= 6 and 2 <= T <= 3, else bypass.
+ * s_out: DEVICE fp32 [num_heads_kv, head_dim].  report: HOST, may be NULL.
+ * workspace: DEVICE, at least hifa4_calibrate_workspace_bytes().
+ * Synchronizes `stream` before returning (an offline call). */
+hifa4_status hifa4_calibrate_smooth_qk(const hifa4_problem* p, int32_t n_calib,
+                                       const void* q_calib, const void* k_calib,
+                                       float alpha, float* s_out,
+                                       hifa4_calib_report* report,
+                                       void* workspace, size_t workspace_bytes,
+                                       void* stream);
+
+/* Smooth-QK then HIF4 quantization of Q~ = fp16(fp32(q)*s) and
+ * K~ = fp16(fp32(k)/s) (IEEE single multiply / correctly rounded divide, one
+ * rounding to fp16), in groups of 64 consecutive channels of each (token,
+ * head) row (Algorithm 1, the Smooth-QK and HIF4 steps).
+ * q, k: DEVICE fp16 in the problem's layout; s: DEVICE fp32
+ * [num_heads_kv, head_dim] or NULL (no smoothing).
+ * Outputs (DEVICE, canonical layout):
+ *   q_codes uint8 [T, num_heads_q, head_dim/64, 32], q_meta uint32 [T, Hq, D/64]
+ *   k_codes uint8 [T, num_heads_kv, head_dim/64, 32], k_meta uint32 [T, Hkv, D/64]
+ * where T is the token count.  Asynchronous. */
+hifa4_status hifa4_quantize_qk(const hifa4_problem* p, const void* q, const void* k,
+                               const float* s, void* q_codes, void* q_meta,
+                               void* k_codes, void* k_meta, void* stream);
+
+/* HIF4 quantization of V along tokens (the contraction axis of PV): groups
+ * of 64 consecutive tokens of one (kv head, channel) column, aligned to each
+ * sequence's first token; a partial last group is zero padded.
+ * v: DEVICE fp16 in the problem's layout.  Outputs (DEVICE, canonical):
+ *   v_codes uint8 [batch, NB, num_heads_kv, head_dim, 32]
+ *   v_meta  uint32 [batch, NB, num_heads_kv, head_dim]
+ * with NB = ceil(max_seqlen/64); groups past a sequence's end are written as
+ * all-zero groups.  Asynchronous. */
+hifa4_status hifa4_quantize_v(const hifa4_problem* p, const void* v, void* v_codes,
+                              void* v_meta, void* stream);
+
+/* The HiFA4 causal prefill forward (Algorithm 1 without Q-Mean; Section 4.5).
+ * q: DEVICE fp16 [.., num_heads_q, head_dim]; k, v: DEVICE fp16
+ * [.., num_heads_kv, head_dim]; s: DEVICE fp32 [num_heads_kv, head_dim] (may be
+ * NULL when opt->smooth_qk == 0 or operands are FP16).
+ * Per query row and 64-key block in ascending order: S2 = fp16(fp32(S*c)),
+ * S the exact HIF4 dot summed over 64-channel groups in fp32,
+ * c = fp32(log2(e)/sqrt(D)); m_new = max(m, rowmax S2); P = fp16(2^(S2-m_new));
+ * r = fp16(2^(m-m_new)); P^ = HIF4(P); O = r*O + P^ V^ and l = r*l + P^ 1
+ * (fp32 accumulation); O_out = fp16(O/l), LSE = m*ln2 + ln(l).
+ * o: DEVICE fp16, same layout as q.  lse: DEVICE fp32 [num_heads_q, T] (T the
+ * token count, natural log of the softmax partition, including the score
+ * scale 1/sqrt(D)).  workspace: DEVICE, >= hifa4_workspace_bytes().
+ * Asynchronous. */
+hifa4_status hifa4_attention_fwd(const hifa4_problem* p, const hifa4_fwd_options* opt,
+                                 const void* q, const void* k, const void* v,
+                                 const float* s, void* o, float* lse,
+                                 void* workspace, size_t workspace_bytes, void* stream);
+
+/* Device self-test of the kernels' fp16 exponential: y[i] = fp16(2^x[i]) for
+ * n fp16 inputs x (DEVICE, fp16 bits), evaluated by the same device routine
+ * the attention kernel uses.  Asynchronous. */
+hifa4_status hifa4_selftest_exp2(const void* x, void* y, int64_t n, void* stream);
+
+/* Message for the last non-OK status returned on the calling thread. */
+const char* hifa4_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HIFA4_H */

@@ -1,0 +1,278 @@
+"""HiFA4 on MI355X: Python binding of libhifa4 (the C ABI in include/hifa4.h).
+
+The binding only marshals arguments: torch tensors supply device memory and
+the current HIP stream; every step of the computation runs in the library's
+HIP kernels.  The shared library is loaded on first use from this package's
+directory and a missing or stale build raises immediately -- there is no
+fallback implementation.
+
+Names mirror the C entry points:
+  hifa4_calibrate_smooth_qk, hifa4_quantize_qk, hifa4_quantize_v,
+  hifa4_attention_fwd, hifa4_workspace_bytes, hifa4_selftest_exp2,
+  hifa4_last_error.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libhifa4.so")
+
+NORM_PREORDER, NORM_INCONSISTENT = 0, 1
+OPERANDS_HIF4, OPERANDS_FP16 = 0, 1
+STATUS = {0: "HIFA4_OK", -1: "HIFA4_ERR_INVALID_ARGUMENT", -2: "HIFA4_ERR_UNSUPPORTED",
+          -3: "HIFA4_ERR_WORKSPACE", -4: "HIFA4_ERR_HIP"}
+
+EXPORTED = ("hifa4_workspace_bytes", "hifa4_calibrate_workspace_bytes", "hifa4_calibrate_smooth_qk",
+            "hifa4_quantize_qk", "hifa4_quantize_v", "hifa4_attention_fwd", "hifa4_selftest_exp2",
+            "hifa4_last_error")
+
+
+class Problem(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("num_heads_q", ctypes.c_int32),
+                ("num_heads_kv", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("max_seqlen", ctypes.c_int32), ("cu_seqlens", ctypes.c_void_p),
+                ("total_tokens", ctypes.c_int32), ("causal", ctypes.c_int32)]
+
+
+class FwdOptions(ctypes.Structure):
+    _fields_ = [("norm", ctypes.c_int32), ("operands", ctypes.c_int32), ("smooth_qk", ctypes.c_int32),
+                ("debug_p_codes", ctypes.c_void_p), ("debug_p_meta", ctypes.c_void_p)]
+
+
+class CalibReport(ctypes.Structure):
+    _fields_ = [("rho_k", ctypes.c_double), ("t_kq", ctypes.c_double), ("branch", ctypes.c_int32),
+                ("alpha_used", ctypes.c_float)]
+
+
+class Hifa4Error(RuntimeError):
+    pass
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libhifa4.so (once).  Raises if it is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"libhifa4.so not found at {path}; build it first "
+                          "(python -m paper_2607_04302_amd.build or __graft_entry__.build())")
+    lib = ctypes.CDLL(path)
+    P = ctypes.POINTER
+    vp, sz = ctypes.c_void_p, ctypes.c_size_t
+    lib.hifa4_workspace_bytes.restype = sz
+    lib.hifa4_workspace_bytes.argtypes = [P(Problem), P(FwdOptions)]
+    lib.hifa4_calibrate_workspace_bytes.restype = sz
+    lib.hifa4_calibrate_workspace_bytes.argtypes = [P(Problem), ctypes.c_int32]
+    lib.hifa4_calibrate_smooth_qk.restype = ctypes.c_int
+    lib.hifa4_calibrate_smooth_qk.argtypes = [P(Problem), ctypes.c_int32, vp, vp, ctypes.c_float, vp,
+                                              P(CalibReport), vp, sz, vp]
+    lib.hifa4_quantize_qk.restype = ctypes.c_int
+    lib.hifa4_quantize_qk.argtypes = [P(Problem), vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.hifa4_quantize_v.restype = ctypes.c_int
+    lib.hifa4_quantize_v.argtypes = [P(Problem), vp, vp, vp, vp]
+    lib.hifa4_attention_fwd.restype = ctypes.c_int
+    lib.hifa4_attention_fwd.argtypes = [P(Problem), P(FwdOptions), vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.hifa4_selftest_exp2.restype = ctypes.c_int
+    lib.hifa4_selftest_exp2.argtypes = [vp, vp, ctypes.c_int64, vp]
+    lib.hifa4_last_error.restype = ctypes.c_char_p
+    lib.hifa4_last_error.argtypes = []
+    _lib = lib
+    return lib
+
+
+def hifa4_last_error() -> str:
+    return load_library().hifa4_last_error().decode()
+
+
+def _check(status: int, what: str):
+    if status != 0:
+        raise Hifa4Error(f"{what}: {STATUS.get(status, status)}: {hifa4_last_error()}")
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(device=None) -> int:
+    torch = _torch()
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _require(t, dtype, name):
+    torch = _torch()
+    if t is None:
+        return
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    del torch
+
+
+@dataclass
+class Shape:
+    batch: int
+    heads_q: int
+    heads_kv: int
+    head_dim: int
+    max_seqlen: int
+    tokens: int
+    cu_seqlens: object = None
+
+    def problem(self) -> Problem:
+        return Problem(self.batch, self.heads_q, self.heads_kv, self.head_dim, self.max_seqlen,
+                       _ptr(self.cu_seqlens), self.tokens if self.cu_seqlens is not None else 0, 1)
+
+
+def shape_of(q, k, cu_seqlens=None, max_seqlen=None) -> Shape:
+    """Problem shape from Q [B,S,Hq,D] (BSHD) or Q [T,Hq,D] + cu_seqlens (THD)."""
+    if cu_seqlens is None:
+        if q.dim() != 4:
+            raise ValueError("fixed-length inputs are [batch, seqlen, heads, dim]")
+        b, s, hq, d = q.shape
+        return Shape(b, hq, k.shape[2], d, s, b * s)
+    if q.dim() != 3:
+        raise ValueError("variable-length inputs are [total_tokens, heads, dim] with cu_seqlens")
+    if max_seqlen is None:
+        raise ValueError("max_seqlen is required with cu_seqlens")
+    _require(cu_seqlens, _torch().int32, "cu_seqlens")
+    t, hq, d = q.shape
+    return Shape(cu_seqlens.numel() - 1, hq, k.shape[1], d, int(max_seqlen), t, cu_seqlens)
+
+
+def hifa4_workspace_bytes(shape: Shape, operands: int = OPERANDS_HIF4) -> int:
+    lib = load_library()
+    p = shape.problem()
+    o = FwdOptions(NORM_PREORDER, operands, 0, None, None)
+    return int(lib.hifa4_workspace_bytes(ctypes.byref(p), ctypes.byref(o)))
+
+
+def hifa4_calibrate_smooth_qk(q_cal, k_cal, alpha: float):
+    """q_cal [n, S, Hq, D], k_cal [n, S, Hkv, D] fp16 on the GPU.  Returns
+    (s fp32 [Hkv, D] on the GPU, report dict).  Synchronizes the stream."""
+    torch = _torch()
+    _require(q_cal, torch.float16, "q_cal")
+    _require(k_cal, torch.float16, "k_cal")
+    lib = load_library()
+    n, s, hq, d = q_cal.shape
+    hkv = k_cal.shape[2]
+    p = Problem(1, hq, hkv, d, s, None, 0, 1)
+    ws_bytes = int(lib.hifa4_calibrate_workspace_bytes(ctypes.byref(p), n))
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=q_cal.device)
+    out = torch.empty((hkv, d), dtype=torch.float32, device=q_cal.device)
+    rep = CalibReport()
+    _check(lib.hifa4_calibrate_smooth_qk(ctypes.byref(p), n, _ptr(q_cal), _ptr(k_cal), float(alpha),
+                                         _ptr(out), ctypes.byref(rep), _ptr(ws), ws_bytes,
+                                         _stream(q_cal.device)), "hifa4_calibrate_smooth_qk")
+    return out, {"rho_k": rep.rho_k, "t_kq": rep.t_kq, "branch": rep.branch, "alpha_used": rep.alpha_used}
+
+
+def hifa4_quantize_qk(q, k, s=None, cu_seqlens=None, max_seqlen=None):
+    """Canonical HIF4 codes of Smooth-QK'd Q and K.  Returns (q_codes uint8
+    [T,Hq,D/64,32], q_meta int32 [T,Hq,D/64], k_codes, k_meta) -- meta words
+    are uint32 bit patterns held in int32 tensors."""
+    torch = _torch()
+    _require(q, torch.float16, "q")
+    _require(k, torch.float16, "k")
+    _require(s, torch.float32, "s")
+    sh = shape_of(q, k, cu_seqlens, max_seqlen)
+    lib = load_library()
+    g = sh.head_dim // 64
+    dev = q.device
+    qc = torch.empty((sh.tokens, sh.heads_q, g, 32), dtype=torch.uint8, device=dev)
+    qm = torch.empty((sh.tokens, sh.heads_q, g), dtype=torch.int32, device=dev)
+    kc = torch.empty((sh.tokens, sh.heads_kv, g, 32), dtype=torch.uint8, device=dev)
+    km = torch.empty((sh.tokens, sh.heads_kv, g), dtype=torch.int32, device=dev)
+    p = sh.problem()
+    _check(lib.hifa4_quantize_qk(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(s), _ptr(qc), _ptr(qm), _ptr(kc),
+                                 _ptr(km), _stream(dev)), "hifa4_quantize_qk")
+    return qc, qm, kc, km
+
+
+def hifa4_quantize_v(v, cu_seqlens=None, max_seqlen=None):
+    """Canonical HIF4 codes of V along tokens: (codes uint8 [B, NB, Hkv, D, 32],
+    meta int32 [B, NB, Hkv, D])."""
+    torch = _torch()
+    _require(v, torch.float16, "v")
+    sh = shape_of(v, v, cu_seqlens, max_seqlen)
+    lib = load_library()
+    nb = (sh.max_seqlen + 63) // 64
+    vc = torch.empty((sh.batch, nb, sh.heads_kv if cu_seqlens is None else v.shape[1], sh.head_dim, 32),
+                     dtype=torch.uint8, device=v.device)
+    sh.heads_kv = vc.shape[2]
+    sh.heads_q = vc.shape[2]
+    vm = torch.empty(vc.shape[:-1], dtype=torch.int32, device=v.device)
+    p = sh.problem()
+    _check(lib.hifa4_quantize_v(ctypes.byref(p), _ptr(v), _ptr(vc), _ptr(vm), _stream(v.device)), "hifa4_quantize_v")
+    return vc, vm
+
+
+class Workspace:
+    """A reusable device workspace (grown on demand)."""
+
+    def __init__(self):
+        self.buf = None
+
+    def get(self, nbytes: int, device):
+        torch = _torch()
+        if self.buf is None or self.buf.numel() < nbytes or self.buf.device != device:
+            self.buf = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+        return self.buf
+
+
+_default_ws = Workspace()
+
+
+def hifa4_attention_fwd(q, k, v, s=None, cu_seqlens=None, max_seqlen=None, norm: int = NORM_PREORDER,
+                        operands: int = OPERANDS_HIF4, smooth_qk: Optional[bool] = None, debug_p: bool = False,
+                        out=None, lse=None, workspace: Optional[Workspace] = None):
+    """HiFA4 causal prefill forward.  Returns (o, lse) or, with debug_p,
+    (o, lse, p_codes uint8 [Hq,T,NB,32], p_meta int32 [Hq,T,NB])."""
+    torch = _torch()
+    for t, n in ((q, "q"), (k, "k"), (v, "v")):
+        _require(t, torch.float16, n)
+    _require(s, torch.float32, "s")
+    sh = shape_of(q, k, cu_seqlens, max_seqlen)
+    lib = load_library()
+    dev = q.device
+    if smooth_qk is None:
+        smooth_qk = s is not None
+    o = torch.empty_like(q) if out is None else out
+    l = torch.empty((sh.heads_q, sh.tokens), dtype=torch.float32, device=dev) if lse is None else lse
+    pc = pm = None
+    if debug_p:
+        nb = (sh.max_seqlen + 63) // 64
+        pc = torch.zeros((sh.heads_q, sh.tokens, nb, 32), dtype=torch.uint8, device=dev)
+        pm = torch.zeros((sh.heads_q, sh.tokens, nb), dtype=torch.int32, device=dev)
+    opt = FwdOptions(norm, operands, 1 if smooth_qk else 0, _ptr(pc), _ptr(pm))
+    p = sh.problem()
+    need = int(lib.hifa4_workspace_bytes(ctypes.byref(p), ctypes.byref(opt)))
+    ws = (workspace or _default_ws).get(need, dev)
+    _check(lib.hifa4_attention_fwd(ctypes.byref(p), ctypes.byref(opt), _ptr(q), _ptr(k), _ptr(v), _ptr(s),
+                                   _ptr(o), _ptr(l), _ptr(ws), ws.numel(), _stream(dev)), "hifa4_attention_fwd")
+    if debug_p:
+        return o, l, pc, pm
+    return o, l
+
+
+def hifa4_selftest_exp2(x):
+    """y = fp16(2^x) through the kernels' exponential routine (x fp16 on GPU)."""
+    torch = _torch()
+    _require(x, torch.float16, "x")
+    y = torch.empty_like(x)
+    _check(load_library().hifa4_selftest_exp2(_ptr(x), _ptr(y), x.numel(), _stream(x.device)), "hifa4_selftest_exp2")
+    return y

@@ -1,0 +1,269 @@
+// C ABI of libhifa4 (declared in include/hifa4.h): argument validation,
+// workspace carving, kernel launches and the host side of calibration.
+#include "../../include/hifa4.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "hifa4_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+hifa4_status fail(hifa4_status st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+hifa4_status fail(hifa4_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+hifa4_status hip_fail(hipError_t e, const char* what) {
+  return fail(HIFA4_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+struct Dims {
+  long tokens;   // rows of the [T, H, D] view
+  int S;         // max_seqlen
+  int NB;        // ceil(S/64)
+};
+
+hifa4_status check_problem(const hifa4_problem* p, Dims* d) {
+  if (!p) return fail(HIFA4_ERR_INVALID_ARGUMENT, "problem is NULL");
+  if (p->batch <= 0 || p->num_heads_q <= 0 || p->num_heads_kv <= 0 || p->max_seqlen < 0)
+    return fail(HIFA4_ERR_INVALID_ARGUMENT, "batch, head counts must be > 0 and max_seqlen >= 0");
+  if (p->num_heads_q % p->num_heads_kv != 0)
+    return fail(HIFA4_ERR_UNSUPPORTED, "num_heads_q (%d) must be a multiple of num_heads_kv (%d)", p->num_heads_q,
+                p->num_heads_kv);
+  if (p->head_dim != 64 && p->head_dim != 128 && p->head_dim != 256)
+    return fail(HIFA4_ERR_UNSUPPORTED, "head_dim %d not in {64, 128, 256}", p->head_dim);
+  if (p->causal != 1) return fail(HIFA4_ERR_UNSUPPORTED, "only causal prefill (causal = 1) is supported");
+  if (p->cu_seqlens && p->total_tokens < 0) return fail(HIFA4_ERR_INVALID_ARGUMENT, "total_tokens < 0");
+  d->S = p->max_seqlen;
+  d->NB = (p->max_seqlen + 63) / 64;
+  d->tokens = p->cu_seqlens ? (long)p->total_tokens : (long)p->batch * p->max_seqlen;
+  if (d->tokens > (1L << 31) / std::max(1, p->num_heads_q))
+    return fail(HIFA4_ERR_UNSUPPORTED, "problem too large for 32-bit row indexing");
+  return HIFA4_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* hifa4_last_error(void) { return g_last_error.c_str(); }
+
+size_t hifa4_workspace_bytes(const hifa4_problem* p, const hifa4_fwd_options* opt) {
+  Dims d;
+  if (check_problem(p, &d) != HIFA4_OK) return 0;
+  const bool fp16 = opt && opt->operands == HIFA4_OPERANDS_FP16;
+  const size_t chunk = fp16 ? hifa4::chunk_layout_fp16(p->head_dim).bytes : hifa4::chunk_layout_hif4(p->head_dim / 64).bytes;
+  return chunk * (size_t)p->batch * p->num_heads_kv * std::max(1, d.NB);
+}
+
+size_t hifa4_calibrate_workspace_bytes(const hifa4_problem* p, int32_t n_calib) {
+  if (!p || n_calib <= 0 || p->num_heads_kv <= 0 || p->head_dim <= 0) return 0;
+  return hifa4::round_up256((size_t)n_calib * 2 * p->num_heads_kv * p->head_dim * 4) + 32768 * 8;
+}
+
+hifa4_status hifa4_quantize_qk(const hifa4_problem* p, const void* q, const void* k, const float* s, void* q_codes,
+                               void* q_meta, void* k_codes, void* k_meta, void* stream) {
+  Dims d;
+  hifa4_status st = check_problem(p, &d);
+  if (st != HIFA4_OK) return st;
+  if (!q || !k || !q_codes || !q_meta || !k_codes || !k_meta)
+    return fail(HIFA4_ERR_INVALID_ARGUMENT, "null tensor pointer");
+  hipStream_t hs = (hipStream_t)stream;
+  using hifa4::half_t;
+  hipError_t e = hifa4::launch_quant_rows((const half_t*)q, s, (uint8_t*)q_codes, (uint32_t*)q_meta, d.tokens,
+                                          p->num_heads_q, p->num_heads_kv, p->head_dim, false, hs);
+  if (e != hipSuccess) return hip_fail(e, "quantize Q");
+  e = hifa4::launch_quant_rows((const half_t*)k, s, (uint8_t*)k_codes, (uint32_t*)k_meta, d.tokens, p->num_heads_kv,
+                               p->num_heads_kv, p->head_dim, true, hs);
+  if (e != hipSuccess) return hip_fail(e, "quantize K");
+  return HIFA4_OK;
+}
+
+hifa4_status hifa4_quantize_v(const hifa4_problem* p, const void* v, void* v_codes, void* v_meta, void* stream) {
+  Dims d;
+  hifa4_status st = check_problem(p, &d);
+  if (st != HIFA4_OK) return st;
+  if (!v || !v_codes || !v_meta) return fail(HIFA4_ERR_INVALID_ARGUMENT, "null tensor pointer");
+  hipError_t e = hifa4::launch_quant_v((const hifa4::half_t*)v, p->cu_seqlens, (uint8_t*)v_codes, (uint32_t*)v_meta,
+                                       p->batch, d.S, d.NB, p->num_heads_kv, p->head_dim, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "quantize V");
+  return HIFA4_OK;
+}
+
+hifa4_status hifa4_attention_fwd(const hifa4_problem* p, const hifa4_fwd_options* opt, const void* q, const void* k,
+                                 const void* v, const float* s, void* o, float* lse, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+  Dims d;
+  hifa4_status st = check_problem(p, &d);
+  if (st != HIFA4_OK) return st;
+  if (!opt) return fail(HIFA4_ERR_INVALID_ARGUMENT, "options is NULL");
+  if (opt->norm != HIFA4_NORM_PREORDER && opt->norm != HIFA4_NORM_INCONSISTENT)
+    return fail(HIFA4_ERR_INVALID_ARGUMENT, "unknown norm %d", opt->norm);
+  if (opt->operands != HIFA4_OPERANDS_HIF4 && opt->operands != HIFA4_OPERANDS_FP16)
+    return fail(HIFA4_ERR_INVALID_ARGUMENT, "unknown operands %d", opt->operands);
+  if (!q || !k || !v || !o || !lse) return fail(HIFA4_ERR_INVALID_ARGUMENT, "null tensor pointer");
+  if ((opt->debug_p_codes == nullptr) != (opt->debug_p_meta == nullptr))
+    return fail(HIFA4_ERR_INVALID_ARGUMENT, "debug_p_codes and debug_p_meta must both be set or both be NULL");
+  const bool fp16 = opt->operands == HIFA4_OPERANDS_FP16;
+  const float* sm = (!fp16 && opt->smooth_qk) ? s : nullptr;
+  if (!fp16 && opt->smooth_qk && !s) return fail(HIFA4_ERR_INVALID_ARGUMENT, "smooth_qk set but s is NULL");
+  if (d.tokens == 0 || d.S == 0) return HIFA4_OK;
+  const size_t need = hifa4_workspace_bytes(p, opt);
+  if (!workspace || workspace_bytes < need)
+    return fail(HIFA4_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required", workspace_bytes, need);
+  hipStream_t hs = (hipStream_t)stream;
+  hipError_t e = hifa4::launch_prep_kv((const hifa4::half_t*)k, (const hifa4::half_t*)v, sm, p->cu_seqlens,
+                                       (uint8_t*)workspace, p->batch, d.S, d.NB, p->num_heads_kv, p->head_dim, fp16, hs);
+  if (e != hipSuccess) return hip_fail(e, "K/V pre-pass");
+  hifa4::AttnArgs a;
+  a.q = (const hifa4::half_t*)q;
+  a.s = sm;
+  a.cu = p->cu_seqlens;
+  a.ws = (const uint8_t*)workspace;
+  a.o = (hifa4::half_t*)o;
+  a.lse = lse;
+  a.dbg_codes = fp16 ? nullptr : (uint8_t*)opt->debug_p_codes;
+  a.dbg_meta = fp16 ? nullptr : (uint32_t*)opt->debug_p_meta;
+  a.batch = p->batch;
+  a.S = d.S;
+  a.NB = d.NB;
+  a.hq = p->num_heads_q;
+  a.hkv = p->num_heads_kv;
+  a.D = p->head_dim;
+  a.total_tokens = (int)d.tokens;
+  a.c = (float)(1.4426950408889634 / std::sqrt((double)p->head_dim));
+  e = hifa4::launch_attention(a, opt->norm, fp16, hs);
+  if (e != hipSuccess) return hip_fail(e, "attention kernel");
+  return HIFA4_OK;
+}
+
+hifa4_status hifa4_selftest_exp2(const void* x, void* y, int64_t n, void* stream) {
+  if (n < 0 || (n > 0 && (!x || !y))) return fail(HIFA4_ERR_INVALID_ARGUMENT, "bad self-test arguments");
+  hipError_t e = hifa4::launch_selftest_exp2((const hifa4::half_t*)x, (hifa4::half_t*)y, (long)n, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "exp2 self-test");
+  return HIFA4_OK;
+}
+
+hifa4_status hifa4_calibrate_smooth_qk(const hifa4_problem* p, int32_t n_calib, const void* q_calib,
+                                       const void* k_calib, float alpha, float* s_out, hifa4_calib_report* report,
+                                       void* workspace, size_t workspace_bytes, void* stream) {
+  if (!p) return fail(HIFA4_ERR_INVALID_ARGUMENT, "problem is NULL");
+  if (n_calib <= 0 || p->max_seqlen <= 0) return fail(HIFA4_ERR_INVALID_ARGUMENT, "n_calib and max_seqlen must be > 0");
+  if (p->num_heads_q <= 0 || p->num_heads_kv <= 0 || p->num_heads_q % p->num_heads_kv)
+    return fail(HIFA4_ERR_UNSUPPORTED, "num_heads_q must be a positive multiple of num_heads_kv");
+  if (p->head_dim != 64 && p->head_dim != 128 && p->head_dim != 256)
+    return fail(HIFA4_ERR_UNSUPPORTED, "head_dim %d not in {64, 128, 256}", p->head_dim);
+  if (!q_calib || !k_calib || !s_out) return fail(HIFA4_ERR_INVALID_ARGUMENT, "null tensor pointer");
+  if (!std::isfinite(alpha) || alpha >= 1.0f) return fail(HIFA4_ERR_INVALID_ARGUMENT, "alpha must be finite and < 1");
+  const size_t need = hifa4_calibrate_workspace_bytes(p, n_calib);
+  if (!workspace || workspace_bytes < need)
+    return fail(HIFA4_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required", workspace_bytes, need);
+  const int hkv = p->num_heads_kv, D = p->head_dim, S = p->max_seqlen;
+  const size_t n_stats = (size_t)n_calib * 2 * hkv * D;
+  uint32_t* stats = (uint32_t*)workspace;
+  unsigned long long* hist = (unsigned long long*)((uint8_t*)workspace + hifa4::round_up256(n_stats * 4));
+  hipStream_t hs = (hipStream_t)stream;
+  hipError_t e = hifa4::launch_calib((const hifa4::half_t*)q_calib, (const hifa4::half_t*)k_calib, n_calib, S,
+                                     p->num_heads_q, hkv, D, stats, hist, hs);
+  if (e != hipSuccess) return hip_fail(e, "calibration kernels");
+  std::vector<uint32_t> hs_stats(n_stats);
+  std::vector<unsigned long long> hh(32768);
+  e = hipMemcpyAsync(hs_stats.data(), stats, n_stats * 4, hipMemcpyDeviceToHost, hs);
+  if (e == hipSuccess) e = hipMemcpyAsync(hh.data(), hist, 32768 * 8, hipMemcpyDeviceToHost, hs);
+  if (e == hipSuccess) e = hipStreamSynchronize(hs);
+  if (e != hipSuccess) return hip_fail(e, "calibration copy-back");
+
+  auto f32 = [](uint32_t u) { float f; std::memcpy(&f, &u, 4); return (double)f; };
+  // RMS over calibration sequences of the per-sequence maxima (float64).
+  std::vector<double> kbar((size_t)hkv * D), qbar((size_t)hkv * D);
+  double kmax_all = 0.0, qmax_all = 0.0;
+  for (size_t i = 0; i < (size_t)hkv * D; ++i) {
+    double sk = 0.0, sq = 0.0;
+    for (int n = 0; n < n_calib; ++n) {
+      const double kv = f32(hs_stats[((size_t)n * 2 + 0) * hkv * D + i]);
+      const double qv = f32(hs_stats[((size_t)n * 2 + 1) * hkv * D + i]);
+      sk += kv * kv;
+      sq += qv * qv;
+      kmax_all = std::max(kmax_all, kv);
+      qmax_all = std::max(qmax_all, qv);
+    }
+    kbar[i] = std::sqrt(sk / n_calib);
+    qbar[i] = std::sqrt(sq / n_calib);
+  }
+  // P99 of |K| with linear interpolation between order statistics.
+  unsigned long long total = 0;
+  for (int i = 0; i < 32768; ++i) total += hh[i];
+  auto order_stat = [&](unsigned long long k) {
+    unsigned long long c = 0;
+    for (int i = 0; i < 32768; ++i) {
+      c += hh[i];
+      if (c > k) {
+        const uint16_t bits = (uint16_t)i;
+        const _Float16 hv = __builtin_bit_cast(_Float16, bits);
+        return (double)(float)hv;
+      }
+    }
+    return 0.0;
+  };
+  double p99 = 0.0;
+  if (total > 0) {
+    const double pos = 0.99 * (double)(total - 1);
+    const unsigned long long lo = (unsigned long long)std::floor(pos);
+    const double t = pos - (double)lo;
+    const double a = order_stat(lo), b = order_stat(std::min(lo + 1, total - 1));
+    const double diff = b - a;
+    p99 = t >= 0.5 ? b - diff * (1.0 - t) : a + diff * t;
+  }
+  const double rho = p99 > 0 ? kmax_all / p99 : INFINITY;
+  const double tkq = qmax_all > 0 ? kmax_all / qmax_all : INFINITY;
+  int branch;
+  double a_used;
+  if (alpha < 0) {
+    if (rho >= 6.0 && tkq > 3.0) branch = 2;
+    else if (rho >= 6.0 && tkq >= 2.0 && tkq <= 3.0) branch = 1;
+    else branch = 0;
+    a_used = branch == 2 ? 0.5 : (branch == 1 ? 0.25 : 0.0);
+  } else if (alpha == 0) {
+    branch = 0;
+    a_used = 0.0;
+  } else {
+    branch = alpha >= 0.5f ? 2 : 1;
+    a_used = alpha;
+  }
+  std::vector<float> sv((size_t)hkv * D, 1.0f);
+  if (a_used != 0.0) {
+    for (size_t i = 0; i < sv.size(); ++i) {
+      const double s = std::pow(kbar[i], a_used) / std::pow(qbar[i], 1.0 - a_used);
+      const bool bad = kbar[i] == 0 || qbar[i] == 0 || !std::isfinite(s) || s == 0;
+      sv[i] = bad ? 1.0f : (float)s;
+    }
+  }
+  e = hipMemcpyAsync(s_out, sv.data(), sv.size() * 4, hipMemcpyHostToDevice, hs);
+  if (e == hipSuccess) e = hipStreamSynchronize(hs);
+  if (e != hipSuccess) return hip_fail(e, "calibration scale upload");
+  if (report) {
+    report->rho_k = rho;
+    report->t_kq = tkq;
+    report->branch = branch;
+    report->alpha_used = (float)a_used;
+  }
+  return HIFA4_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,165 @@
+// Device-side building blocks shared by the HiFA4 kernels (gfx950).
+//
+// HIF4 group quantization (paper, Background "HIF4" paragraph; Section 4.1)
+// under the library's reading: unsigned E6M2 base b = smallest value with
+// 1.75*b >= max|x| (bias 31); level-2 (8 elements) and level-3 (4 elements)
+// one-bit micro-exponents that halve the scale when the block's maximum fits
+// in half of the range; element code u = round-half-away(|x| / step),
+// step = b * 2^-(E2+E3) / 4.
+//
+// MFMA operand encoding.  A HIF4 element equals o * b/4 with o = u * 2^-sh,
+// u in 0..7 and sh = E2+E3 in 0..2.  Every such o is exactly representable in
+// the OCP FP6 E2M3 format (values m/8 and (1+m/8)*2^(e-1)), which E2M1 (FP4)
+// cannot hold (5 and 7 need three significant bits).  The kernels therefore
+// feed o as FP6 E2M3 to the block-scaled F8F6F4 MFMA (same issue rate as
+// FP4) with unit E8M0 scales, so every group dot product sum(o_q * o_k) is
+// exact in the fp32 accumulator, and apply the E6M2 bases (which carry two
+// mantissa bits that an E8M0 scale cannot) in an fp32 epilogue.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hifa4 {
+
+typedef _Float16 half_t;
+typedef _Float16 h2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 h8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 h32_t __attribute__((ext_vector_type(32)));
+typedef float f16v_t __attribute__((ext_vector_type(16)));
+typedef int i6_t __attribute__((ext_vector_type(6)));
+typedef int i8_t __attribute__((ext_vector_type(8)));
+
+// FP6 E2M3 encoding of 1.0 (sign 0, exponent 01, mantissa 000), replicated
+// in 6-bit fields: the all-ones operand of the fused normalizer [V^ | 1].
+constexpr uint32_t kE2M3One = 0x08;
+
+// E6M2 value of a base byte: (1 + m/4) * 2^(e - 31).
+__device__ __forceinline__ float e6m2_value(uint32_t code) {
+  return __builtin_ldexpf(1.0f + 0.25f * (float)(code & 3u), (int)(code >> 2) - 31);
+}
+
+// Smallest E6M2 byte whose value b satisfies 1.75*b >= A (A >= 0, an fp16 or
+// fp16-softmax value held exactly in fp32).  A first guess comes from
+// A*(4/7) rounded up to two mantissa bits; the two exact comparisons below
+// (1.75*b is exact in fp32) correct the at most one-step error of the guess.
+__device__ __forceinline__ uint32_t e6m2_ceil(float A) {
+  if (!(A > 0.0f)) return 0u;
+  const float T = A * (4.0f / 7.0f);
+  const uint32_t bits = __float_as_uint(T);
+  int code = (((int)((bits >> 23) & 255u) - 127 + 31) << 2) | (int)((bits >> 21) & 3u);
+  if (bits & 0x1FFFFFu) code += 1;
+  code = code < 0 ? 0 : (code > 255 ? 255 : code);
+  if (code > 0 && 1.75f * e6m2_value((uint32_t)(code - 1)) >= A) code -= 1;
+  if (code < 255 && 1.75f * e6m2_value((uint32_t)code) < A) code += 1;
+  return (uint32_t)code;
+}
+
+// R = (4/b) * (1 + 2^-18), rounded: for the 4 base mantissas the constant
+// fp32(16/(4+m) * (1 + 2^-18)), then an exact power-of-two scaling.
+//
+// Element rounding uses o = fl(a*R + C_sh) - C_sh with C_sh = 1.5*2^(23-sh):
+// the fused multiply-add rounds the exact product a*R once onto the grid
+// 2^-sh, which is u*2^-sh with u = round-half-to-even(a/step * (1+beta)).
+// a/step is an fp16 value divided by (4+m)*2^k: a non-tie lies at least
+// 2^-12 (relative) from a half-integer while beta ~ 2^-18, so those round as
+// exactly as without beta; an exact tie n+1/2 is pushed strictly above and
+// rounds away from zero.  The result is exactly round-half-away(a/step).
+__device__ __forceinline__ float hif4_rcp_step(uint32_t code) {
+  const uint32_t m = code & 3u;
+  const float r = m == 0 ? 0x1.00004p+2f
+                : m == 1 ? 0x1.999ap+1f
+                : m == 2 ? 0x1.5555aap+1f
+                         : 0x1.249292p+1f;
+  return __builtin_ldexpf(r, 31 - (int)(code >> 2));
+}
+
+__device__ __forceinline__ float round_const(int sh) {
+  return sh == 0 ? 12582912.0f : (sh == 1 ? 6291456.0f : 3145728.0f);
+}
+
+// o = u * 2^-sh for one element magnitude a (>= 0).
+__device__ __forceinline__ float hif4_elem(float a, float R, float C) {
+  return __builtin_fmaf(a, R, C) - C;
+}
+
+// fp16 softmax exponential E(x) = fp16(2^x) for a pair of fp16 x (x = -inf
+// gives 0), as v_exp_f16 on each half.  On gfx950 it returns the correctly
+// rounded value for every fp16 input x <= 0 (checked exhaustively; the
+// library's exp2 self-test entry point re-checks it on the device).
+__device__ __forceinline__ h2_t exp2_h2(h2_t x) { return __builtin_elementwise_exp2(x); }
+
+__device__ __forceinline__ float shfl_xor32(float v) {
+  return __shfl_xor(v, 32);
+}
+__device__ __forceinline__ uint32_t shfl_xor32_u(uint32_t v) {
+  return (uint32_t)__shfl_xor((int)v, 32);
+}
+
+// ---------------------------------------------------------------------------
+// Lane-split group quantization.  A 64-element group is held by a lane pair
+// (lane l and l^32), 32 elements each, as 8 complete 4-element blocks.
+// `q4[k]` is the global index (0..15) of the lane's k-th 4-block, and a4[k]
+// its maximum magnitude.  Both lanes compute identical group metadata.
+struct GroupMeta {
+  uint32_t base;    // E6M2 byte
+  uint32_t e2;      // 8 bits
+  uint32_t e3;      // 16 bits
+  float b;          // base value
+};
+
+// a4_all[0..15]: the maxima of all 16 4-blocks of the group, in block order.
+__device__ __forceinline__ GroupMeta group_meta(const float a4_all[16]) {
+  GroupMeta g;
+  float A8[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) A8[j] = fmaxf(a4_all[2 * j], a4_all[2 * j + 1]);
+  float A = A8[0];
+#pragma unroll
+  for (int j = 1; j < 8; ++j) A = fmaxf(A, A8[j]);
+  g.base = e6m2_ceil(A);
+  g.b = e6m2_value(g.base);
+  const float half_range = 0.875f * g.b;
+  g.e2 = 0;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) g.e2 |= (A8[j] <= half_range ? 1u : 0u) << j;
+  g.e3 = 0;
+#pragma unroll
+  for (int q = 0; q < 16; ++q) {
+    const float lim = ((g.e2 >> (q >> 1)) & 1u) ? 0.5f * half_range : half_range;
+    g.e3 |= (a4_all[q] <= lim ? 1u : 0u) << q;
+  }
+  return g;
+}
+
+__device__ __forceinline__ int block_shift(const GroupMeta& g, int q4) {
+  return (int)((g.e2 >> (q4 >> 1)) & 1u) + (int)((g.e3 >> q4) & 1u);
+}
+
+// Which 4-blocks a lane holds.  kRows: lane half h holds the contiguous
+// elements [32h, 32h+32), i.e. blocks 8h..8h+7 (Q, K along channels).
+// kKeys: the lane's k-th block is (t = k/4, j = k%4), elements
+// 32t + 8j + 4h + [0,4), i.e. block 8t + 2j + h (V along tokens, and P,
+// following the 32x32 MFMA output layout of S^T).
+enum { kRows = 0, kKeys = 1 };
+
+template <int LAYOUT>
+__device__ __forceinline__ int own_block(int k, int h) {
+  return LAYOUT == kRows ? 8 * h + k : 8 * (k >> 2) + 2 * (k & 3) + h;
+}
+
+// Assemble the 16 block maxima of the group from the lane's 8 and its
+// partner's (lane l^32) 8, with static register indexing.
+template <int LAYOUT>
+__device__ __forceinline__ void gather_a4(const float own[8], float all[16], int h) {
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const float other = shfl_xor32(own[k]);
+    const int lo = LAYOUT == kRows ? k : 8 * (k >> 2) + 2 * (k & 3);
+    const int hi = LAYOUT == kRows ? 8 + k : lo + 1;
+    all[lo] = h ? other : own[k];
+    all[hi] = h ? own[k] : other;
+  }
+}
+
+}  // namespace hifa4

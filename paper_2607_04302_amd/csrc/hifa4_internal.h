@@ -1,0 +1,67 @@
+// Internal declarations shared by the HIP translation units of libhifa4.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace hifa4 {
+
+typedef _Float16 half_t;
+
+// Byte layout of one pre-pass chunk = (sequence, kv head, 64-key block).
+// Offsets are multiples of 256 bytes.
+struct ChunkLayout {
+  size_t k_op, k_scale, v_op, v_scale, bytes;
+};
+
+__host__ __device__ constexpr size_t round_up256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// HIF4 operands: K [2][G][64][24 B], K scales [2][G][32] fp32,
+// V [D/32][64][24 B], V scales [D] fp32.
+__host__ __device__ constexpr ChunkLayout chunk_layout_hif4(int G) {
+  ChunkLayout c{};
+  c.k_op = 0;
+  c.k_scale = round_up256((size_t)2 * G * 64 * 24);
+  c.v_op = c.k_scale + round_up256((size_t)2 * G * 32 * 4);
+  c.v_scale = c.v_op + round_up256((size_t)(2 * G) * 64 * 24);
+  c.bytes = c.v_scale + round_up256((size_t)64 * G * 4);
+  return c;
+}
+
+// FP16 operands: K [2][D/16][64][16 B], V [D/32][4][64][16 B].
+__host__ __device__ constexpr ChunkLayout chunk_layout_fp16(int D) {
+  ChunkLayout c{};
+  c.k_op = 0;
+  c.k_scale = c.k_op + round_up256((size_t)2 * (D / 16) * 64 * 16);
+  c.v_op = c.k_scale;
+  c.v_scale = c.v_op + round_up256((size_t)(D / 32) * 4 * 64 * 16);
+  c.bytes = c.v_scale;
+  return c;
+}
+
+struct AttnArgs {
+  const half_t* q;
+  const float* s;          // smoothing scales or nullptr
+  const int* cu;           // cu_seqlens or nullptr
+  const uint8_t* ws;       // pre-pass chunks
+  half_t* o;
+  float* lse;
+  uint8_t* dbg_codes;      // optional P^ dump
+  uint32_t* dbg_meta;
+  int batch, S, NB, hq, hkv, D, total_tokens;
+  float c;                 // log2(e)/sqrt(D)
+};
+
+hipError_t launch_quant_rows(const half_t* x, const float* s, uint8_t* codes, uint32_t* meta, long n_rows,
+                             int heads, int heads_kv, int D, bool is_k, hipStream_t st);
+hipError_t launch_quant_v(const half_t* v, const int* cu, uint8_t* codes, uint32_t* meta, int batch, int S, int NB,
+                          int heads_kv, int D, hipStream_t st);
+hipError_t launch_prep_kv(const half_t* k, const half_t* v, const float* s, const int* cu, uint8_t* ws, int batch,
+                          int S, int NB, int heads_kv, int D, bool fp16, hipStream_t st);
+hipError_t launch_calib(const half_t* q, const half_t* k, int n, int S, int hq, int hkv, int D, uint32_t* stats,
+                        unsigned long long* hist, hipStream_t st);
+hipError_t launch_selftest_exp2(const half_t* x, half_t* y, long n, hipStream_t st);
+hipError_t launch_attention(const AttnArgs& a, int norm, bool fp16, hipStream_t st);
+
+}  // namespace hifa4

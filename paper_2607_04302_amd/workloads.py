@@ -139,7 +139,7 @@ def small_case(heads_q=2, heads_kv=1, head_dim=128, seqlens=(200,), seed=7,
                outlier_channels=(5, 77), outlier_scale=16.0):
     """A small seeded case for parity tests (varlen layout if several lengths)."""
     w = Workload("small", len(seqlens), heads_q, heads_kv, head_dim, max(seqlens),
-                 outlier_fixed=tuple(outlier_channels) if outlier_channels else (),
+                 outlier_fixed=tuple(c % head_dim for c in outlier_channels) if outlier_channels else (),
                  outlier_scale=outlier_scale)
     rng = np.random.default_rng(seed)
     t = int(sum(seqlens))

@@ -1,0 +1,71 @@
+"""C ABI: the library loads, exports every entry point of include/hifa4.h, and
+rejects invalid arguments with status codes before any GPU work."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_04302_amd as h
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    text = open(os.path.join(ROOT, "include", "hifa4.h")).read()
+    return sorted(set(re.findall(r"\b(hifa4_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_and_binding_agree():
+    assert set(_declared()) == set(h.EXPORTED)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(h.LIB_PATH):
+        pytest.skip("libhifa4.so not built")
+    return h.load_library()
+
+
+def test_exports(lib):
+    for name in _declared():
+        assert hasattr(lib, name), name
+
+
+def _p(**kw):
+    base = dict(batch=1, num_heads_q=4, num_heads_kv=2, head_dim=128, max_seqlen=128,
+                cu_seqlens=None, total_tokens=0, causal=1)
+    base.update(kw)
+    return h.Problem(**base)
+
+
+def _fwd(lib, p, opt=None, ptr=1, ws=1 << 30):
+    opt = opt or h.FwdOptions(0, 0, 0, None, None)
+    return lib.hifa4_attention_fwd(ctypes.byref(p), ctypes.byref(opt), ptr, ptr, ptr, None, ptr, ptr,
+                                   ptr, ws, None)
+
+
+def test_validation_codes(lib):
+    assert _fwd(lib, _p(head_dim=96)) == -2
+    assert "head_dim" in h.hifa4_last_error()
+    assert _fwd(lib, _p(num_heads_q=3, num_heads_kv=2)) == -2
+    assert _fwd(lib, _p(causal=0)) == -2
+    assert _fwd(lib, _p(batch=0)) == -1
+    assert _fwd(lib, _p(), ptr=None) == -1
+    assert _fwd(lib, _p(), opt=h.FwdOptions(7, 0, 0, None, None)) == -1
+    assert _fwd(lib, _p(), opt=h.FwdOptions(0, 0, 1, None, None)) == -1      # smooth without s
+    assert _fwd(lib, _p(), opt=h.FwdOptions(0, 0, 0, 1, None)) == -1         # half a debug dump
+    assert _fwd(lib, _p(), ws=16) == -3
+    assert "workspace" in h.hifa4_last_error()
+    assert lib.hifa4_selftest_exp2(None, None, -1, None) == -1
+
+
+def test_workspace_sizes(lib):
+    p = _p(max_seqlen=4096, num_heads_q=32, num_heads_kv=8)
+    o = h.FwdOptions(0, 0, 0, None, None)
+    n = lib.hifa4_workspace_bytes(ctypes.byref(p), ctypes.byref(o))
+    # 64 blocks x 8 kv heads x (6 KB K op + 512 B scales + 6 KB V op + 512 B)
+    assert n == 64 * 8 * 13312
+    o16 = h.FwdOptions(0, 1, 0, None, None)
+    assert lib.hifa4_workspace_bytes(ctypes.byref(p), ctypes.byref(o16)) == 64 * 8 * 32768
+    assert lib.hifa4_workspace_bytes(ctypes.byref(_p(head_dim=80)), ctypes.byref(o)) == 0

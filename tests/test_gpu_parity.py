@@ -1,0 +1,198 @@
+"""GPU parity: the HIP path against the CPU oracle on the same seeded inputs.
+
+Bit-exact: the kernels' fp16 exponential (all inputs), Q^/K^/V^ codes and
+metadata, and every P^ group written by the attention kernel's debug dump.
+Tolerance (element-wise |gpu - ref| <= 2e-3 + 1e-2*|ref|): O and LSE."""
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import attention as oatt
+from oracle import hif4 as ohif4
+from oracle import smooth as osmooth
+from oracle.softmax16 import exp2_fp16
+from paper_2607_04302_amd.workloads import WORKLOADS, make_calibration, make_inputs, small_case
+
+from _gpu_util import check_close, to_gpu, to_np
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def h():
+    import paper_2607_04302_amd as mod
+    mod.load_library()
+    return mod
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def test_exp2_exhaustive(h):
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    x = bits.view(np.float16)
+    sel = (np.isfinite(x) & (x <= 0)) | (x == -np.inf)
+    xs = x[sel]
+    got = to_np(h.hifa4_selftest_exp2(to_gpu(xs)))
+    want = exp2_fp16(xs)
+    assert np.array_equal(got.view(np.uint16), want.view(np.uint16))
+
+
+@pytest.mark.parametrize("d,hq,hkv,lens", [(128, 4, 2, (200,)), (64, 2, 2, (77, 130)), (256, 2, 1, (96,))])
+def test_quantize_qk_bitexact(h, d, hq, hkv, lens):
+    q, k, v, cu = small_case(heads_q=hq, heads_kv=hkv, head_dim=d, seqlens=lens, seed=d + hq)
+    s = np.exp(np.random.default_rng(1).uniform(-2, 2, (hkv, d))).astype(np.float32)
+    for sv in (None, s):
+        qc, qm, kc, km = oatt.quantize_qk(q, k, sv)
+        cu_t = to_gpu(cu)
+        g = h.hifa4_quantize_qk(to_gpu(q), to_gpu(k), None if sv is None else to_gpu(sv),
+                                cu_seqlens=cu_t, max_seqlen=max(lens))
+        assert np.array_equal(to_np(g[0]), qc)
+        assert np.array_equal(to_np(g[1]).view(np.uint32), qm)
+        assert np.array_equal(to_np(g[2]), kc)
+        assert np.array_equal(to_np(g[3]).view(np.uint32), km)
+
+
+def _canon_v_padded(v, cu, nb):
+    """Oracle V^ codes in the padded [B, NB, Hkv, D] layout."""
+    hkv, d = v.shape[1], v.shape[2]
+    codes = np.zeros((len(cu) - 1, nb, hkv, d, 32), np.uint8)
+    meta = np.zeros((len(cu) - 1, nb, hkv, d), np.uint32)
+    for b in range(len(cu) - 1):
+        for hk in range(hkv):
+            f, _ = oatt.quantize_tokens(v[cu[b]:cu[b + 1], hk])        # [D, G_b, 64]
+            c_, m_ = ohif4.pack(f)
+            gb = c_.shape[1]
+            codes[b, :gb, hk] = c_.transpose(1, 0, 2)
+            meta[b, :gb, hk] = m_.T
+        # groups past the end are all-zero groups
+        zc, zm = ohif4.pack(ohif4.quantize(np.zeros(64)))
+        gb = -(-(cu[b + 1] - cu[b]) // 64)
+        codes[b, gb:] = zc
+        meta[b, gb:] = zm
+    return codes, meta
+
+
+def test_quantize_v_bitexact(h):
+    q, k, v, cu = small_case(heads_q=2, heads_kv=2, head_dim=128, seqlens=(200, 64, 1, 129), seed=3)
+    nb = -(-200 // 64)
+    g = h.hifa4_quantize_v(to_gpu(v), cu_seqlens=to_gpu(cu), max_seqlen=200)
+    codes, meta = _canon_v_padded(v, cu, nb)
+    assert np.array_equal(to_np(g[0]), codes)
+    assert np.array_equal(to_np(g[1]).view(np.uint32), meta)
+
+
+def _run_and_compare(h, q, k, v, cu, s, max_seqlen, norm="preorder", heads=None, rows=None, check_p=True):
+    cu_t = None if cu is None else to_gpu(cu)
+    nm = h.NORM_PREORDER if norm == "preorder" else h.NORM_INCONSISTENT
+    o, lse, pc, pm = h.hifa4_attention_fwd(to_gpu(q), to_gpu(k), to_gpu(v), None if s is None else to_gpu(s),
+                                           cu_seqlens=cu_t, max_seqlen=max_seqlen, norm=nm, debug_p=True)
+    o, lse, pc, pm = to_np(o), to_np(lse), to_np(pc), to_np(pm).view(np.uint32)
+    ref = oatt.attention_fwd(q, k, v, s, cu_seqlens=cu, norm=norm, heads=heads, rows=rows, want_p=True)
+    if cu is None:
+        bsz, S = q.shape[:2]
+        cuv = np.arange(bsz + 1) * S
+        o = o.reshape(bsz * S, *o.shape[2:])
+    else:
+        cuv = cu
+    worst = 0.0
+    for (b, hh), r in ref.items():
+        tok = cuv[b] + r["rows"]
+        worst = max(worst, check_close(o[tok, hh], r["o"], what=f"O seq {b} head {hh}"))
+        check_close(lse[hh, tok], r["lse"], atol=2e-3, rtol=0, what="LSE")
+        if check_p:
+            for ii, i in enumerate(r["rows"]):
+                nb_i = i // 64 + 1
+                assert np.array_equal(pc[hh, tok[ii], :nb_i], r["p_codes"][ii, :nb_i]), (b, hh, i)
+                assert np.array_equal(pm[hh, tok[ii], :nb_i], r["p_meta"][ii, :nb_i]), (b, hh, i)
+    return worst
+
+
+def test_tiny_config_full_parity(h):
+    """The tiny causal prefill workload (S=256, D=128) with Smooth-QK scales
+    from its 4-sequence calibration draw: every P^ code bit-exact, O, LSE."""
+    w = WORKLOADS["tiny_s256"]
+    q, k, v, _ = make_inputs(w)
+    qc, kc = make_calibration(w)
+    s, _ = osmooth.calibrate(qc, kc, w.heads_kv, w.alpha)
+    _say("tiny_s256 preorder")
+    err = _run_and_compare(h, q, k, v, None, s, w.seqlen)
+    _say("tiny_s256 max err", err)
+    _say("tiny_s256 inconsistent")
+    _run_and_compare(h, q, k, v, None, s, w.seqlen, norm="inconsistent")
+
+
+@pytest.mark.parametrize("d,hq,hkv,lens,seed", [
+    (128, 4, 1, (300, 65, 64, 1, 190), 1),      # GQA x4, ragged tails, single token
+    (64, 2, 2, (129, 511), 2),                   # no GQA, D=64
+    (256, 4, 2, (200, 33), 3),                   # GQA x2, D=256
+    (128, 8, 8, (97,), 4),
+])
+def test_varlen_parity(h, d, hq, hkv, lens, seed):
+    q, k, v, cu = small_case(heads_q=hq, heads_kv=hkv, head_dim=d, seqlens=lens, seed=seed)
+    s = np.exp(np.random.default_rng(seed).uniform(-1, 1.5, (hkv, d))).astype(np.float32)
+    _say("varlen", d, hq, hkv, lens)
+    _run_and_compare(h, q, k, v, cu, s, max(lens))
+    _run_and_compare(h, q, k, v, cu, None, max(lens), norm="inconsistent")
+
+
+def test_fp16_variant(h):
+    q, k, v, cu = small_case(heads_q=4, heads_kv=2, head_dim=128, seqlens=(300, 47), seed=9)
+    for d in (64, 128, 256):
+        q, k, v, cu = small_case(heads_q=4, heads_kv=2, head_dim=d, seqlens=(300, 47), seed=9)
+        _say("fp16 variant D", d)
+        o, lse = h.hifa4_attention_fwd(to_gpu(q), to_gpu(k), to_gpu(v), None, cu_seqlens=to_gpu(cu),
+                                       max_seqlen=300, operands=h.OPERANDS_FP16)
+        o, lse = to_np(o), to_np(lse)
+        ref = oatt.attention_fwd(q, k, v, None, cu_seqlens=cu, operands="fp16")
+        for (b, hh), r in ref.items():
+            tok = cu[b] + r["rows"]
+            check_close(o[tok, hh], r["o"], what="fp16 O")
+            check_close(lse[hh, tok], r["lse"], atol=2e-3, rtol=0, what="fp16 LSE")
+
+
+def test_constant_v_invariant(h):
+    """A constant V row comes back bit-exactly under P-Reordering; the
+    inconsistent normalizer scales it by (1 + eps) (Theorem 1 with e_t = 0)."""
+    q, k, v, cu = small_case(heads_q=2, heads_kv=1, head_dim=128, seqlens=(333,), seed=9)
+    v[:] = v[0, 0]
+    _, vhat = oatt.quantize_tokens(v[:, 0])
+    target = vhat[0].astype(np.float16)
+    o, _ = h.hifa4_attention_fwd(to_gpu(q), to_gpu(k), to_gpu(v), None, cu_seqlens=to_gpu(cu), max_seqlen=333)
+    o = to_np(o)
+    assert np.array_equal(o, np.broadcast_to(target, o.shape))
+    om, _ = h.hifa4_attention_fwd(to_gpu(q), to_gpu(k), to_gpu(v), None, cu_seqlens=to_gpu(cu), max_seqlen=333,
+                                  norm=h.NORM_INCONSISTENT)
+    om = to_np(om)
+    assert (om != np.broadcast_to(target, om.shape)).mean() > 0.5
+
+
+def test_calibration(h):
+    w = WORKLOADS["tiny_s256"]
+    qc, kc = make_calibration(w)
+    for alpha in (0.5, 0.25, 0.0, -1.0):
+        s_ref, rep = osmooth.calibrate(qc, kc, w.heads_kv, alpha)
+        s_gpu, grep = h.hifa4_calibrate_smooth_qk(to_gpu(qc), to_gpu(kc), alpha)
+        s_gpu = to_np(s_gpu)
+        # same float64 formulas on both sides; allow one fp32 ulp for libm pow
+        ulp = np.abs(s_gpu.view(np.int32).astype(np.int64) - s_ref.view(np.int32).astype(np.int64))
+        assert ulp.max() <= 1, alpha
+        assert abs(grep["rho_k"] - rep["rho_k"]) < 1e-9 * rep["rho_k"]
+        assert abs(grep["t_kq"] - rep["t_kq"]) < 1e-12 * rep["t_kq"]
+        assert grep["branch"] == rep["branch"]
+
+
+def test_qwen3_shape_sampled(h):
+    """Qwen3-8B-shaped S=4096 workload at full size, in the launch the
+    benchmark times: sampled heads (one per KV group plus neighbours) and
+    rows spanning the first, middle and last blocks, P^ codes bit-exact."""
+    w = WORKLOADS["qwen3_8b_s4096"]
+    q, k, v, _ = make_inputs(w)
+    qc, kc = make_calibration(w, n=4)
+    s, _ = osmooth.calibrate(qc, kc, w.heads_kv, w.alpha)
+    rows = [0, 1, 31, 63, 64, 65, 1000, 2047, 2048, 3071, 4031, 4094, 4095]
+    _say("qwen3 sampled")
+    _run_and_compare(h, q, k, v, None, s, w.seqlen, heads=[0, 3, 4, 17, 31], rows=rows)
