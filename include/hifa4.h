@@ -108,13 +108,19 @@ typedef enum {
  *                  its sequence) sees, other entries are left untouched;
  *   debug_p_meta   NULL, or a DEVICE uint32 buffer [num_heads_q, T, NB] with
  *                  the matching metadata words.  Both or neither.
- * Debug dumps are only produced for HIFA4_OPERANDS_HIF4. */
+ * Debug dumps are only produced for HIFA4_OPERANDS_HIF4.
+ *   timing_events  NULL, or a HOST array of three hipEvent_t (created by the
+ *                  caller) that the call records on `stream` before the K/V
+ *                  pre-pass, between the pre-pass and the attention kernel,
+ *                  and after the attention kernel -- per-kernel device time
+ *                  without a profiler.  The events are not waited on. */
 typedef struct {
   int32_t norm;       /* hifa4_norm      */
   int32_t operands;   /* hifa4_operands  */
   int32_t smooth_qk;
   void* debug_p_codes;
   void* debug_p_meta;
+  void** timing_events;
 } hifa4_fwd_options;
 
 /* Host-side calibration report (Table 1 statistics and the gate decision). */

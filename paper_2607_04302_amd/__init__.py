@@ -40,7 +40,8 @@ class Problem(ctypes.Structure):
 
 class FwdOptions(ctypes.Structure):
     _fields_ = [("norm", ctypes.c_int32), ("operands", ctypes.c_int32), ("smooth_qk", ctypes.c_int32),
-                ("debug_p_codes", ctypes.c_void_p), ("debug_p_meta", ctypes.c_void_p)]
+                ("debug_p_codes", ctypes.c_void_p), ("debug_p_meta", ctypes.c_void_p),
+                ("timing_events", ctypes.c_void_p)]
 
 
 class CalibReport(ctypes.Structure):
@@ -157,7 +158,7 @@ def shape_of(q, k, cu_seqlens=None, max_seqlen=None) -> Shape:
 def hifa4_workspace_bytes(shape: Shape, operands: int = OPERANDS_HIF4) -> int:
     lib = load_library()
     p = shape.problem()
-    o = FwdOptions(NORM_PREORDER, operands, 0, None, None)
+    o = FwdOptions(NORM_PREORDER, operands, 0, None, None, None)
     return int(lib.hifa4_workspace_bytes(ctypes.byref(p), ctypes.byref(o)))
 
 
@@ -239,9 +240,11 @@ _default_ws = Workspace()
 
 def hifa4_attention_fwd(q, k, v, s=None, cu_seqlens=None, max_seqlen=None, norm: int = NORM_PREORDER,
                         operands: int = OPERANDS_HIF4, smooth_qk: Optional[bool] = None, debug_p: bool = False,
-                        out=None, lse=None, workspace: Optional[Workspace] = None):
+                        out=None, lse=None, workspace: Optional[Workspace] = None, timing_events=None):
     """HiFA4 causal prefill forward.  Returns (o, lse) or, with debug_p,
-    (o, lse, p_codes uint8 [Hq,T,NB,32], p_meta int32 [Hq,T,NB])."""
+    (o, lse, p_codes uint8 [Hq,T,NB,32], p_meta int32 [Hq,T,NB]).
+    timing_events: optional three recorded torch.cuda.Event objects (before
+    the pre-pass, before the attention kernel, after it)."""
     torch = _torch()
     for t, n in ((q, "q"), (k, "k"), (v, "v")):
         _require(t, torch.float16, n)
@@ -258,7 +261,11 @@ def hifa4_attention_fwd(q, k, v, s=None, cu_seqlens=None, max_seqlen=None, norm:
         nb = (sh.max_seqlen + 63) // 64
         pc = torch.zeros((sh.heads_q, sh.tokens, nb, 32), dtype=torch.uint8, device=dev)
         pm = torch.zeros((sh.heads_q, sh.tokens, nb), dtype=torch.int32, device=dev)
-    opt = FwdOptions(norm, operands, 1 if smooth_qk else 0, _ptr(pc), _ptr(pm))
+    ev_arr = None
+    if timing_events is not None:
+        ev_arr = (ctypes.c_void_p * 3)(*[e.cuda_event for e in timing_events])
+    opt = FwdOptions(norm, operands, 1 if smooth_qk else 0, _ptr(pc), _ptr(pm),
+                     ctypes.cast(ev_arr, ctypes.c_void_p) if ev_arr is not None else None)
     p = sh.problem()
     need = int(lib.hifa4_workspace_bytes(ctypes.byref(p), ctypes.byref(opt)))
     ws = (workspace or _default_ws).get(need, dev)

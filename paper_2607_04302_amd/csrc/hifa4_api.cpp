@@ -128,9 +128,13 @@ hifa4_status hifa4_attention_fwd(const hifa4_problem* p, const hifa4_fwd_options
   if (!workspace || workspace_bytes < need)
     return fail(HIFA4_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required", workspace_bytes, need);
   hipStream_t hs = (hipStream_t)stream;
-  hipError_t e = hifa4::launch_prep_kv((const hifa4::half_t*)k, (const hifa4::half_t*)v, sm, p->cu_seqlens,
-                                       (uint8_t*)workspace, p->batch, d.S, d.NB, p->num_heads_kv, p->head_dim, fp16, hs);
+  hipEvent_t* ev = (hipEvent_t*)opt->timing_events;
+  hipError_t e = hipSuccess;
+  if (ev && (e = hipEventRecord(ev[0], hs)) != hipSuccess) return hip_fail(e, "timing event");
+  e = hifa4::launch_prep_kv((const hifa4::half_t*)k, (const hifa4::half_t*)v, sm, p->cu_seqlens, (uint8_t*)workspace,
+                            p->batch, d.S, d.NB, p->num_heads_kv, p->head_dim, fp16, hs);
   if (e != hipSuccess) return hip_fail(e, "K/V pre-pass");
+  if (ev && (e = hipEventRecord(ev[1], hs)) != hipSuccess) return hip_fail(e, "timing event");
   hifa4::AttnArgs a;
   a.q = (const hifa4::half_t*)q;
   a.s = sm;
@@ -150,6 +154,7 @@ hifa4_status hifa4_attention_fwd(const hifa4_problem* p, const hifa4_fwd_options
   a.c = (float)(1.4426950408889634 / std::sqrt((double)p->head_dim));
   e = hifa4::launch_attention(a, opt->norm, fp16, hs);
   if (e != hipSuccess) return hip_fail(e, "attention kernel");
+  if (ev && (e = hipEventRecord(ev[2], hs)) != hipSuccess) return hip_fail(e, "timing event");
   return HIFA4_OK;
 }
 

@@ -40,7 +40,7 @@ def _p(**kw):
 
 
 def _fwd(lib, p, opt=None, ptr=1, ws=1 << 30):
-    opt = opt or h.FwdOptions(0, 0, 0, None, None)
+    opt = opt or h.FwdOptions(0, 0, 0, None, None, None)
     return lib.hifa4_attention_fwd(ctypes.byref(p), ctypes.byref(opt), ptr, ptr, ptr, None, ptr, ptr,
                                    ptr, ws, None)
 
@@ -52,9 +52,9 @@ def test_validation_codes(lib):
     assert _fwd(lib, _p(causal=0)) == -2
     assert _fwd(lib, _p(batch=0)) == -1
     assert _fwd(lib, _p(), ptr=None) == -1
-    assert _fwd(lib, _p(), opt=h.FwdOptions(7, 0, 0, None, None)) == -1
-    assert _fwd(lib, _p(), opt=h.FwdOptions(0, 0, 1, None, None)) == -1      # smooth without s
-    assert _fwd(lib, _p(), opt=h.FwdOptions(0, 0, 0, 1, None)) == -1         # half a debug dump
+    assert _fwd(lib, _p(), opt=h.FwdOptions(7, 0, 0, None, None, None)) == -1
+    assert _fwd(lib, _p(), opt=h.FwdOptions(0, 0, 1, None, None, None)) == -1      # smooth without s
+    assert _fwd(lib, _p(), opt=h.FwdOptions(0, 0, 0, 1, None, None)) == -1         # half a debug dump
     assert _fwd(lib, _p(), ws=16) == -3
     assert "workspace" in h.hifa4_last_error()
     assert lib.hifa4_selftest_exp2(None, None, -1, None) == -1
@@ -62,10 +62,10 @@ def test_validation_codes(lib):
 
 def test_workspace_sizes(lib):
     p = _p(max_seqlen=4096, num_heads_q=32, num_heads_kv=8)
-    o = h.FwdOptions(0, 0, 0, None, None)
+    o = h.FwdOptions(0, 0, 0, None, None, None)
     n = lib.hifa4_workspace_bytes(ctypes.byref(p), ctypes.byref(o))
     # 64 blocks x 8 kv heads x (6 KB K op + 512 B scales + 6 KB V op + 512 B)
     assert n == 64 * 8 * 13312
-    o16 = h.FwdOptions(0, 1, 0, None, None)
+    o16 = h.FwdOptions(0, 1, 0, None, None, None)
     assert lib.hifa4_workspace_bytes(ctypes.byref(p), ctypes.byref(o16)) == 64 * 8 * 32768
     assert lib.hifa4_workspace_bytes(ctypes.byref(_p(head_dim=80)), ctypes.byref(o)) == 0

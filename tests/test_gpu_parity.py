@@ -140,7 +140,6 @@ def test_varlen_parity(h, d, hq, hkv, lens, seed):
 
 
 def test_fp16_variant(h):
-    q, k, v, cu = small_case(heads_q=4, heads_kv=2, head_dim=128, seqlens=(300, 47), seed=9)
     for d in (64, 128, 256):
         q, k, v, cu = small_case(heads_q=4, heads_kv=2, head_dim=d, seqlens=(300, 47), seed=9)
         _say("fp16 variant D", d)
@@ -150,8 +149,13 @@ def test_fp16_variant(h):
         ref = oatt.attention_fwd(q, k, v, None, cu_seqlens=cu, operands="fp16")
         for (b, hh), r in ref.items():
             tok = cu[b] + r["rows"]
-            check_close(o[tok, hh], r["o"], what="fp16 O")
-            check_close(lse[hh, tok], r["lse"], atol=2e-3, rtol=0, what="fp16 LSE")
+            # The FP16 reference sums q.k in fp32 in the MFMA's own order, so a
+            # score can round to the neighbouring fp16 value (one ulp: 2^-11
+            # relative); that scales one weight by 2^(2^-7) ~ 1.0054 at
+            # |S2| < 16 and moves O by up to 0.54% of |v - O| for that key, and
+            # LSE by up to ulp(m)*ln2 ~ 1e-3*|LSE|.
+            check_close(o[tok, hh], r["o"], atol=1e-2, rtol=1e-2, what="fp16 O")
+            check_close(lse[hh, tok], r["lse"], atol=2e-3, rtol=1e-3, what="fp16 LSE")
 
 
 def test_constant_v_invariant(h):
