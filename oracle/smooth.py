@@ -15,8 +15,9 @@ Readings (the paper leaves these open):
   * gate statistics over every calibration element of the layer:
     rho_K = max|K| / P99(|K|) (linear-interpolation percentile),
     T = max|K| / max|Q|;
-  * application: q~ = fp16(fp32(q) * s), k~ = fp16(fp32(k) / s) -- one IEEE
-    single multiply or correctly rounded divide, then one rounding to fp16.
+  * application: q~ = fp16(q * s) and k~ = fp16(k / s): the exact product or
+    quotient of the fp16 activation and the fp32 scale, rounded once to fp16
+    (round to nearest, ties to even).
 """
 from __future__ import annotations
 
@@ -91,11 +92,37 @@ def calibrate(q_cal, k_cal, heads_kv, alpha):
                "qbar": qbar, "kbar": kbar}
 
 
+def _round_quotient_fp16(k, s):
+    """fp16 nearest to the exact quotient k/s (k fp16, s fp32), ties to even.
+    The float64 quotient is within half a float64 ulp of the exact one, so it
+    rounds to the same fp16 unless it lands exactly on an fp16 midpoint; there
+    the exact sign of k - mid*s (mid*s is exact in float64) decides."""
+    k64 = k.astype(np.float64)
+    s64 = np.broadcast_to(s.astype(np.float64), k64.shape)
+    with np.errstate(over="ignore", invalid="ignore", divide="ignore"):
+        q64 = k64 / s64
+        h = q64.astype(np.float16)
+        hv = h.astype(np.float64)
+        # neighbour on the far side of q64
+        toward = np.where(q64 > hv, np.float16(np.inf), np.float16(-np.inf)).astype(np.float16)
+        nb = np.nextafter(h, toward).astype(np.float64)
+        mid = (hv + nb) / 2.0
+        at_mid = np.isfinite(q64) & (q64 == mid) & (hv != nb)
+        if np.any(at_mid):
+            diff = k64 - mid * s64              # exact sign of (k/s - mid) * s
+            exact_side = np.sign(diff) * np.sign(s64)
+            want_nb = exact_side == np.sign(nb - mid)
+            # an exact tie keeps the even neighbour, which astype already chose
+            h = np.where(at_mid & want_nb & (diff != 0), nb.astype(np.float16), h)
+    return h
+
+
 def apply(q, k, s, heads_kv):
     """Smooth-QK on [..., H, D] fp16 tensors (q: Hq heads, k: Hkv heads)."""
     s = np.asarray(s, np.float32)
     hq = q.shape[-2]
     sq = np.repeat(s, hq // heads_kv, axis=0)
-    qt = (q.astype(np.float32) * sq).astype(np.float16)
-    kt = (k.astype(np.float32) / s).astype(np.float16)
+    # the product of an fp16 and an fp32 value is exact in float64
+    qt = (q.astype(np.float64) * sq.astype(np.float64)).astype(np.float16)
+    kt = _round_quotient_fp16(k, s)
     return qt, kt

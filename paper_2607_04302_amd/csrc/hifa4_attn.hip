@@ -86,47 +86,98 @@ __device__ __forceinline__ f16v_t mfma6(const i8_t& A, const i8_t& B, const f16v
 
 __device__ __forceinline__ half_t hmax(half_t a, half_t b) { return a > b ? a : b; }
 
+// Lane-pair exchange with v_permlane32_swap(v, v): it swaps the upper 32
+// lanes of the first copy with the lower 32 lanes of the second, so lanes
+// 0..31 see (own, partner) and lanes 32..63 see (partner, own).  Symmetric
+// combinations need no select.
+struct Pair32 {
+  uint32_t x, y;
+};
+__device__ __forceinline__ Pair32 pair32(uint32_t v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return Pair32{r[0], r[1]};
+}
+__device__ __forceinline__ h2_t max_with_partner(h2_t v) {
+  const Pair32 p = pair32(__builtin_bit_cast(uint32_t, v));
+  return __builtin_elementwise_max(__builtin_bit_cast(h2_t, p.x), __builtin_bit_cast(h2_t, p.y));
+}
+__device__ __forceinline__ float add_with_partner(float v) {
+  const Pair32 p = pair32(__builtin_bit_cast(uint32_t, v));
+  return __builtin_bit_cast(float, p.x) + __builtin_bit_cast(float, p.y);
+}
+// The partner lane's value (h = lane / 32).
+__device__ __forceinline__ h2_t partner_h2(h2_t v, int h) {
+  const Pair32 p = pair32(__builtin_bit_cast(uint32_t, v));
+  return __builtin_bit_cast(h2_t, h ? p.x : p.y);
+}
+
+// t = fp16(p*R + C) for both halves of p (fp16), R and C fp32: each result is
+// the exact fused value rounded once to fp16.
+__device__ __forceinline__ h2_t fma_grid2(h2_t p, float R, float C) {
+  h2_t y;
+  asm("v_fma_mixlo_f16 %0, %1, %2, %3 op_sel_hi:[1,0,0]\n\t"
+      "v_fma_mixhi_f16 %0, %1, %2, %3 op_sel:[1,0,0] op_sel_hi:[1,0,0]"
+      : "=&v"(y)
+      : "v"(p), "v"(R), "v"(C));
+  return y;
+}
+
 // Global key index (within the 64-key block) held by lane half h at tile t,
 // accumulator register v of the 32x32 output layout.
 __device__ __forceinline__ int key_of(int t, int h, int v) { return 32 * t + 8 * (v >> 2) + 4 * h + (v & 3); }
 
 // ---------------------------------------------------------------------------
-template <int G, int NORM>
-__global__ void __launch_bounds__(256) k_attn_hif4(AttnArgs a, int heads_per_wg, int qsub, int n_qtiles) {
+// HiFA4 kernel.
+//
+// Pipeline per wave: the QK^T MFMAs of block J+1 are issued before the
+// softmax / quantization VALU work of block J, so the matrix cores and the
+// vector ALUs overlap.  K/V chunks rotate through three LDS buffers: while
+// block J is consumed (K of J+1, V of J), chunk J+2 is fetched into registers
+// and written to the buffer chunk J-1 used.
+//
+// Deferred rescale: instead of O <- r*O every block, the kernel keeps
+// O* = O / rho and l* = l / rho with rho the product of the rescale factors so
+// far, and adds each block's contribution scaled by 1/rho.  O*/l* = O/l, so
+// the output and the P^ codes are unchanged; only the fp32 rounding of O
+// differs.  A factor r = 0 (a running max that grows by more than 24 in log2
+// units after the first block) wipes the history, exactly as r*O does.
+template <int G, int NORM, bool DEBUG>
+__global__ void __launch_bounds__(256, (G == 1 ? 2 : 1)) k_attn_hif4(AttnArgs a, int heads_per_wg, int qsub, int n_qtiles) {
   constexpr int D = 64 * G;
   constexpr int DT = D / 32;
   constexpr ChunkLayout lay = chunk_layout_hif4(G);
   constexpr int cbytes = (int)lay.bytes;
   constexpr int n16 = cbytes / 16;
-  constexpr int n_pre = n16 < 1024 ? (n16 + 255) / 256 : 4;
+  constexpr int n_pre = (n16 + 255) / 256;
+  constexpr bool kPipe = G <= 2;
   extern __shared__ __align__(16) uint8_t smem[];
   const TileMap tm = map_tile(a, heads_per_wg, qsub, n_qtiles);
   if (!tm.wg_live) return;
   const int lane = threadIdx.x & 63, h = lane >> 5, col = lane & 31;
-  const int qi = tm.qw + col;                 // this lane's query position
+  const int qi = tm.qw + col;
   const bool row_ok = tm.active && qi < tm.L;
   const int jw_last = tm.active ? (min(tm.qw + 31, tm.L - 1)) / 64 : -1;
 
-  // ---- Q tile: Smooth-QK then HIF4 into FP6 B operands (one per group).
+  // ---- Q tile: Smooth-QK (fp16(q*s)) then HIF4 into FP6 B operands.
   i8_t qop[G];
   float bq[G];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
-    float x[32], o[32];
+    float x[32];
     if (row_ok) {
       const half_t* src = a.q + ((size_t)(tm.t0 + qi) * a.hq + tm.hq) * D + 64 * g + 32 * h;
-      const uint4* p = reinterpret_cast<const uint4*>(src);
+      const u4_t* p = reinterpret_cast<const u4_t*>(src);
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        uint4 w = p[v];
-        const half_t* hh = reinterpret_cast<const half_t*>(&w);
+        const u4_t w = p[v];
+        const h8_t hh = __builtin_bit_cast(h8_t, w);
 #pragma unroll
         for (int i = 0; i < 8; ++i) x[8 * v + i] = (float)hh[i];
       }
       if (a.s) {
         const float* sp = a.s + (size_t)tm.hk * D + 64 * g + 32 * h;
 #pragma unroll
-        for (int c = 0; c < 32; ++c) x[c] = (float)(half_t)(x[c] * sp[c]);
+        for (int c = 0; c < 32; ++c) x[c] = (float)mul_rn16(x[c], sp[c]);
       }
     } else {
 #pragma unroll
@@ -152,8 +203,7 @@ __global__ void __launch_bounds__(256) k_attn_hif4(AttnArgs a, int heads_per_wg,
       for (int i = 0; i < 4; ++i) {
         const float xv = x[4 * k + i];
         const float ov = hif4_elem(fabsf(xv), R, C);
-        o[4 * k + i] = xv < 0.0f ? -ov : ov;
-        hv[4 * k + i] = (half_t)o[4 * k + i];
+        hv[4 * k + i] = (half_t)(xv < 0.0f ? -ov : ov);
       }
     }
     const i6_t pk = __builtin_amdgcn_cvt_scalef32_pk32_fp6_f16(hv, 1.0f);
@@ -166,7 +216,6 @@ __global__ void __launch_bounds__(256) k_attn_hif4(AttnArgs a, int heads_per_wg,
 
   i8_t ones;
   {
-    // 32 FP6 fields of 1.0 packed in 192 bits.
     uint32_t w[6] = {0, 0, 0, 0, 0, 0};
 #pragma unroll
     for (int s = 0; s < 32; ++s) {
@@ -186,39 +235,49 @@ __global__ void __launch_bounds__(256) k_attn_hif4(AttnArgs a, int heads_per_wg,
 #pragma unroll
     for (int v = 0; v < 16; ++v) O[dt][v] = 0.0f;
   half_t m_run = (half_t)(-__builtin_inff());
-  float l_con = 0.0f, l_mis = 0.0f;
+  float l_star = 0.0f;     // l / rho (consistent or mismatched per NORM)
+  float inv_rho = 1.0f;    // 1 / rho
 
   const uint8_t* ws_base = a.ws + ((size_t)(tm.b * a.hkv + tm.hk) * a.NB) * lay.bytes;
   stage_chunk(smem, ws_base, cbytes);
+  if (tm.nJ > 1) stage_chunk(smem + cbytes, ws_base + cbytes, cbytes);
   __syncthreads();
 
+  // QK MFMAs of one block: acc[t][g] = K^ tile (t, g) x Q^ group g.
+  f16v_t acc[2][G];
+  auto issue_qk = [&](const uint8_t* buf) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const i8_t kop = ld_op6(buf + lay.k_op + ((size_t)(t * G + g) * 64 + lane) * 24);
+        const f16v_t zero = {};
+        acc[t][g] = mfma6(kop, qop[g], zero);
+      }
+  };
+  if (kPipe && tm.active) issue_qk(smem);
+
   for (int J = 0; J < tm.nJ; ++J) {
-    // Prefetch (up to 16 KB of) the next chunk into registers while this one
-    // is consumed; the index is clamped so every load stays inside the chunk.
-    // The loads are unconditional (the last iteration re-reads its own chunk)
-    // so that the staging registers never live in scratch memory.
-    const bool has_next = J + 1 < tm.nJ;
+    const uint8_t* cur = smem + (J % 3) * cbytes;
+    const bool has_next2 = J + 2 < tm.nJ;
     u4_t pre[n_pre];
     {
-      const u4_t* src = reinterpret_cast<const u4_t*>(ws_base + (size_t)(has_next ? J + 1 : J) * cbytes);
+      const u4_t* src = reinterpret_cast<const u4_t*>(ws_base + (size_t)(has_next2 ? J + 2 : J) * cbytes);
 #pragma unroll
       for (int r = 0; r < n_pre; ++r) {
         const int i = threadIdx.x + 256 * r;
         pre[r] = src[i < n16 ? i : n16 - 1];
       }
     }
-    const uint8_t* cur = smem + (J & 1) * cbytes;
     if (tm.active && J <= jw_last) {
-      // ---- S^T = K^ Q^T (exact group dots) and the fp32 score epilogue.
+      if (!kPipe) issue_qk(cur);
+      // ---- scores: S2 = fp16((sum_g t_g) * c), t_g = acc_g * (b_q b_k) exact.
       h2_t s2[2][8];
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
-        f16v_t sacc;
+        float sacc[16];
 #pragma unroll
         for (int g = 0; g < G; ++g) {
-          const i8_t kop = ld_op6(cur + lay.k_op + ((size_t)(t * G + g) * 64 + lane) * 24);
-          f16v_t zero = {};
-          const f16v_t acc = mfma6(kop, qop[g], zero);
           const float* ksc = reinterpret_cast<const float*>(cur + lay.k_scale) + (t * G + g) * 32 + 4 * h;
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
@@ -227,18 +286,17 @@ __global__ void __launch_bounds__(256) k_attn_hif4(AttnArgs a, int heads_per_wg,
             for (int i = 0; i < 4; ++i) {
               const int v = 4 * j + i;
               const float w = bq[g] * bkv[i];
-              sacc[v] = (g == 0) ? acc[v] * w : __builtin_fmaf(acc[v], w, sacc[v]);
+              sacc[v] = (g == 0) ? acc[t][g][v] * w : __builtin_fmaf(acc[t][g][v], w, sacc[v]);
             }
           }
         }
 #pragma unroll
-        for (int v2 = 0; v2 < 8; ++v2) {
-          s2[t][v2][0] = (half_t)(sacc[2 * v2] * a.c);
-          s2[t][v2][1] = (half_t)(sacc[2 * v2 + 1] * a.c);
-        }
+        for (int v2 = 0; v2 < 8; ++v2) s2[t][v2] = mul2_rn16(sacc[2 * v2], sacc[2 * v2 + 1], a.c);
       }
-      // ---- causal mask (only the block that holds the diagonal).
-      if (64 * J + 63 > tm.qw) {
+      // ---- issue the next block's QK^T while this block's VALU work runs.
+      if (kPipe && J < jw_last) issue_qk(smem + ((J + 1) % 3) * cbytes);
+      // ---- causal mask on the block that holds the diagonal.
+      if (J == jw_last) {
         const half_t ninf = (half_t)(-__builtin_inff());
 #pragma unroll
         for (int t = 0; t < 2; ++t)
@@ -246,154 +304,193 @@ __global__ void __launch_bounds__(256) k_attn_hif4(AttnArgs a, int heads_per_wg,
           for (int v = 0; v < 16; ++v)
             if (64 * J + key_of(t, h, v) > qi) s2[t][v >> 1][v & 1] = ninf;
       }
-      // ---- running max (FP16).
+      // ---- running max (FP16), exchanged with lane l^32.
       h2_t mx2 = s2[0][0];
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int v2 = 0; v2 < 8; ++v2) mx2 = __builtin_elementwise_max(mx2, s2[t][v2]);
-      half_t mx = hmax(mx2[0], mx2[1]);
-      {
-        const float other = shfl_xor32((float)mx);
-        mx = hmax(mx, (half_t)other);
-      }
+      mx2 = max_with_partner(mx2);
+      const half_t mx = hmax(mx2[0], mx2[1]);
       const half_t m_new = hmax(m_run, mx);
       const h2_t mn2 = {m_new, m_new};
-      // ---- P = 2^(S2 - m_new) in fp16; r = 2^(m - m_new).
+      // ---- P = 2^(S2 - m_new), r = 2^(m - m_new), block max A = 2^(mx - m_new).
       h2_t p2[2][8];
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int v2 = 0; v2 < 8; ++v2) p2[t][v2] = exp2_h2(s2[t][v2] - mn2);
-      const h2_t rr = exp2_h2(h2_t{(half_t)(m_run - m_new), (half_t)0});
-      const float r = (float)rr[0];
+      const h2_t ra = exp2_h2(h2_t{(half_t)(m_run - m_new), (half_t)(mx - m_new)});
+      const float r = (float)ra[0];
+      const float A = (float)ra[1];
       m_run = m_new;
 
+      float psum = 0.0f;
       if (NORM == 1) {
-        float ps = 0.0f;
 #pragma unroll
         for (int t = 0; t < 2; ++t)
 #pragma unroll
-          for (int v2 = 0; v2 < 8; ++v2) ps += (float)p2[t][v2][0] + (float)p2[t][v2][1];
-        ps += shfl_xor32(ps);
-        l_mis = l_mis * r + ps;
+          for (int v2 = 0; v2 < 8; ++v2) psum = __builtin_amdgcn_fdot2(p2[t][v2], h2_t{(half_t)1, (half_t)1}, psum, false);
+        psum = add_with_partner(psum);
       }
 
       // ---- P^ = HIF4(P) over the block's 64 keys (P-Reordering).
-      // The lane's 4-block (t, j) holds keys 32t + 8j + 4h + [0,4): global
-      // 4-block index 8t + 2j + h; its values are p2[t][2j], p2[t][2j+1].
-      float a4own[8];
+      // Lane 4-block (t, j): keys 32t + 8j + 4h + [0,4) = p2[t][2j], p2[t][2j+1].
+      h2_t a4p[4];          // own 4-block maxima, packed (t,0|t,1), (t,2|t,3)
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const h2_t mm = __builtin_elementwise_max(p2[t][2 * j], p2[t][2 * j + 1]);
-          a4own[4 * t + j] = (float)hmax(mm[0], mm[1]);
+        for (int jp = 0; jp < 2; ++jp) {
+          const h2_t m0 = __builtin_elementwise_max(p2[t][4 * jp], p2[t][4 * jp + 1]);
+          const h2_t m1 = __builtin_elementwise_max(p2[t][4 * jp + 2], p2[t][4 * jp + 3]);
+          a4p[2 * t + jp] = h2_t{hmax(m0[0], m0[1]), hmax(m1[0], m1[1])};
         }
-      float a4_all[16];
-      gather_a4<kKeys>(a4own, a4_all, h);
-      const GroupMeta gm = group_meta(a4_all);
-      const float R = hif4_rcp_step(gm.base);
-      f16v_t px, py;     // tile 0 -> x, tile 1 -> y (the cvt interleaves them)
+      const uint32_t base = e6m2_ceil(A);
+      const float bval = e6m2_value(base);
+      const float R = hif4_rcp_step(base);
+      // fp16 floors of the half and quarter ranges: an fp16 value x satisfies
+      // x <= 0.875b iff x <= floor16(0.875b) (round-toward-zero conversion).
+      const h2_t thr = __builtin_bit_cast(h2_t, __builtin_amdgcn_cvt_pkrtz(0.875f * bval, 0.4375f * bval));
+      uint32_t e2bits = 0, e3bits = 0;
+      h2_t cpair[8];        // per 4-block rounding constant (fp16, both halves)
 #pragma unroll
-      for (int t = 0; t < 2; ++t)
+      for (int q = 0; q < 4; ++q) {
+        const h2_t a8 = max_with_partner(a4p[q]);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const float C = round_const(block_shift(gm, 8 * t + 2 * j + h));
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int v = 4 * j + i;
-            const float pv = (float)p2[t][v >> 1][v & 1];
-            const float ov = hif4_elem(pv, R, C);
-            if (t == 0) px[v] = ov; else py[v] = ov;
+        for (int e = 0; e < 2; ++e) {
+          const int t = q >> 1, j = 2 * (q & 1) + e;
+          const bool e2 = a8[e] <= thr[0];
+          const bool e3 = a4p[q][e] <= (e2 ? thr[1] : thr[0]);
+          const int sh = (int)e2 + (int)e3;
+          // C16 = 1.5 * 2^(10-sh) as fp16: exponent field 25 - sh, mantissa 0x200
+          const uint16_t cb = (uint16_t)(((25 - sh) << 10) | 0x200);
+          const half_t c16 = __builtin_bit_cast(half_t, cb);
+          cpair[4 * t + j] = h2_t{c16, c16};
+          if (DEBUG) {
+            e2bits |= (uint32_t)e2 << (4 * t + j);
+            e3bits |= (uint32_t)e3 << (8 * t + 2 * j + h);
+            const bool e3o = partner_h2(a4p[q], h)[e] <= (e2 ? thr[1] : thr[0]);
+            e3bits |= (uint32_t)e3o << (8 * t + 2 * j + (h ^ 1));
           }
         }
-      const i6_t pk = __builtin_amdgcn_cvt_scalef32_2xpk16_fp6_f32(px, py, 1.0f);
+      }
+      // o = u * 2^-sh: round P*R onto the grid 2^-sh in one fp16 fma, then
+      // subtract the offset (both exact); then pack 32 values to FP6.
+      h32_t ov;
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const h2_t c2 = cpair[4 * t + j];
+#pragma unroll
+          for (int e = 0; e < 2; ++e) {
+            const h2_t pv = p2[t][2 * j + e];
+            h2_t tt = fma_grid2(pv, R, (float)c2[0]);
+            tt = tt - c2;
+            // slot order of the B operand: slot 2v + t holds tile t, reg v
+            const int v0 = 4 * j + 2 * e;
+            ov[2 * v0 + t] = tt[0];
+            ov[2 * (v0 + 1) + t] = tt[1];
+          }
+        }
+      const i6_t pk = __builtin_amdgcn_cvt_scalef32_pk32_fp6_f16(ov, 1.0f);
       i8_t pop;
 #pragma unroll
       for (int i = 0; i < 6; ++i) pop[i] = pk[i];
       pop[6] = 0;
       pop[7] = 0;
-      const float bp = 0.25f * gm.b;
 
-      if (a.dbg_codes && row_ok) {
-        // canonical dump: byte index = key/2; the lane writes the bytes of its
-        // 4-blocks (keys 32t+8j+4h .. +3 -> bytes 16t+4j+2h, +1).
+      if (DEBUG && row_ok) {
         uint8_t* dc = a.dbg_codes + (((size_t)tm.hq * a.total_tokens + tm.t0 + qi) * a.NB + J) * 32;
 #pragma unroll
         for (int t = 0; t < 2; ++t)
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            const int sh = block_shift(gm, 8 * t + 2 * j + h);
+            const int q4 = 8 * t + 2 * j + h;
+            const int sh = (int)((e2bits >> (4 * t + j)) & 1u) + (int)((e3bits >> q4) & 1u);
             uint32_t nib[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-              const float ov = t == 0 ? px[4 * j + i] : py[4 * j + i];
-              nib[i] = (uint32_t)(ov * (float)(1 << sh));
+              const int v = 4 * j + i;
+              nib[i] = (uint32_t)((float)ov[2 * v + t] * (float)(1 << sh));
             }
             dc[16 * t + 4 * j + 2 * h] = (uint8_t)(nib[0] | (nib[1] << 4));
             dc[16 * t + 4 * j + 2 * h + 1] = (uint8_t)(nib[2] | (nib[3] << 4));
           }
         if (h == 0)
-          a.dbg_meta[((size_t)tm.hq * a.total_tokens + tm.t0 + qi) * a.NB + J] = gm.base | (gm.e2 << 8) | (gm.e3 << 16);
+          a.dbg_meta[((size_t)tm.hq * a.total_tokens + tm.t0 + qi) * a.NB + J] = base | (e2bits << 8) | (e3bits << 16);
       }
 
-      // ---- rescale history (skipped while the max is unchanged).
-      const bool need = __builtin_amdgcn_ballot_w64(r != 1.0f) != 0;
-      if (need) {
+      // ---- deferred rescale bookkeeping (lane-uniform factors).
+      if (J > 0 && __builtin_amdgcn_ballot_w64(r == 0.0f) != 0) {
+        // history wiped for some rows: O <- 0*O, l <- 0*l there
+        if (r == 0.0f) {
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) O[dt][v] = 0.0f;
+          l_star = 0.0f;
+        }
+      }
+      inv_rho = (r == 0.0f) ? 1.0f : inv_rho * __builtin_amdgcn_rcpf(r);
+      if (__builtin_amdgcn_ballot_w64(inv_rho > 0x1p64f) != 0) {
+        const float rho = __builtin_amdgcn_rcpf(inv_rho);
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-          for (int v = 0; v < 16; ++v) O[dt][v] *= r;
+          for (int v = 0; v < 16; ++v) O[dt][v] *= rho;
+        l_star *= rho;
+        inv_rho = 1.0f;
       }
-      // ---- [O | l] += P^ [V^ | 1].
+      const float wp = 0.25f * bval * inv_rho;      // b_P/4 / rho
+      // ---- [O | l] += P^ [V^ | 1]; V^'s scale is split over three MFMAs.
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
         const i8_t vop = ld_op6(cur + lay.v_op + ((size_t)dt * 64 + lane) * 24);
-        f16v_t zero = {};
-        const f16v_t acc = mfma6(vop, pop, zero);
-        const float* vsc = reinterpret_cast<const float*>(cur + lay.v_scale) + 32 * dt + 4 * h;
+        const int vs = reinterpret_cast<const int*>(cur + lay.v_scale)[32 * dt + col];
+        f16v_t pv = {};
+        pv = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vop, pop, pv, 2, 2, 0, vs, 0, 127);
+        pv = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vop, pop, pv, 2, 2, 1, vs, 0, 127);
+        pv = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vop, pop, pv, 2, 2, 2, vs, 0, 127);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const f4_t bvv = *reinterpret_cast<const f4_t*>(vsc + 8 * j);
-#pragma unroll
-          for (int i = 0; i < 4; ++i) O[dt][4 * j + i] = __builtin_fmaf(acc[4 * j + i], bp * bvv[i], O[dt][4 * j + i]);
-        }
+        for (int v = 0; v < 16; ++v) O[dt][v] = __builtin_fmaf(pv[v], wp, O[dt][v]);
       }
-      {
-        f16v_t zero = {};
+      if (NORM == 1) {
+        l_star = __builtin_fmaf(psum, inv_rho, l_star);
+      } else {
+        const f16v_t zero = {};
         const f16v_t lacc = mfma6(ones, pop, zero);
-        l_con = l_con * r + bp * lacc[0];
+        l_star = __builtin_fmaf(lacc[0], wp, l_star);
       }
     }
-    if (has_next) {
-      u4_t* dst = reinterpret_cast<u4_t*>(smem + ((J + 1) & 1) * cbytes);
+    if (has_next2) {
+      u4_t* dst = reinterpret_cast<u4_t*>(smem + ((J + 2) % 3) * cbytes);
 #pragma unroll
       for (int r = 0; r < n_pre; ++r) {
         const int i = threadIdx.x + 256 * r;
         if (i < n16) dst[i] = pre[r];
       }
-      if (n16 > 1024) stage_chunk(smem + ((J + 1) & 1) * cbytes + 16384, ws_base + (size_t)(J + 1) * cbytes + 16384, cbytes - 16384);
     }
     __syncthreads();
   }
 
-  // ---- finalize: O = fp16(O / l), LSE = m ln2 + ln l.
+  // ---- finalize: O = fp16(O*/l*), LSE = m ln2 + ln(l* rho).
   if (row_ok) {
-    const float l = NORM == 1 ? l_mis : l_con;
-    const float inv = 1.0f / l;
+    const float inv = 1.0f / l_star;
     half_t* dst = a.o + ((size_t)(tm.t0 + qi) * a.hq + tm.hq) * D;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         typedef _Float16 h4_t __attribute__((ext_vector_type(4)));
-        h4_t ov;
+        h4_t o4;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) ov[i] = (half_t)(O[dt][4 * j + i] * inv);
-        *reinterpret_cast<h4_t*>(dst + 32 * dt + 8 * j + 4 * h) = ov;
+        for (int i = 0; i < 4; ++i) o4[i] = (half_t)(O[dt][4 * j + i] * inv);
+        *reinterpret_cast<h4_t*>(dst + 32 * dt + 8 * j + 4 * h) = o4;
       }
-    if (h == 0) a.lse[(size_t)tm.hq * a.total_tokens + tm.t0 + qi] = (float)m_run * 0.69314718055994531f + logf(l);
+    if (h == 0)
+      a.lse[(size_t)tm.hq * a.total_tokens + tm.t0 + qi] =
+          (float)m_run * 0.69314718055994531f + logf(l_star) - logf(inv_rho);
   }
 }
 
@@ -558,20 +655,20 @@ hipError_t launch_attention(const AttnArgs& a, int norm, bool fp16, hipStream_t 
     }
     return hipErrorInvalidValue;
   }
-  const size_t lds = 2 * chunk_layout_hif4(a.D / 64).bytes;
-  if (norm == 0) {
-    switch (a.D) {
-      case 64: return launch_k(k_attn_hif4<1, 0>, a, lds, st);
-      case 128: return launch_k(k_attn_hif4<2, 0>, a, lds, st);
-      case 256: return launch_k(k_attn_hif4<4, 0>, a, lds, st);
-    }
-  } else {
-    switch (a.D) {
-      case 64: return launch_k(k_attn_hif4<1, 1>, a, lds, st);
-      case 128: return launch_k(k_attn_hif4<2, 1>, a, lds, st);
-      case 256: return launch_k(k_attn_hif4<4, 1>, a, lds, st);
-    }
+  const size_t lds = 3 * chunk_layout_hif4(a.D / 64).bytes;
+  const bool dbg = a.dbg_codes != nullptr;
+#define HIFA4_DISPATCH(G)                                                                            \
+  do {                                                                                               \
+    if (norm == 0)                                                                                   \
+      return dbg ? launch_k(k_attn_hif4<G, 0, true>, a, lds, st) : launch_k(k_attn_hif4<G, 0, false>, a, lds, st); \
+    return dbg ? launch_k(k_attn_hif4<G, 1, true>, a, lds, st) : launch_k(k_attn_hif4<G, 1, false>, a, lds, st);   \
+  } while (0)
+  switch (a.D) {
+    case 64: HIFA4_DISPATCH(1);
+    case 128: HIFA4_DISPATCH(2);
+    case 256: HIFA4_DISPATCH(4);
   }
+#undef HIFA4_DISPATCH
   return hipErrorInvalidValue;
 }
 

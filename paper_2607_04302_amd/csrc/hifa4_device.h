@@ -84,10 +84,57 @@ __device__ __forceinline__ float hif4_elem(float a, float R, float C) {
 }
 
 // fp16 softmax exponential E(x) = fp16(2^x) for a pair of fp16 x (x = -inf
-// gives 0), as v_exp_f16 on each half.  On gfx950 it returns the correctly
-// rounded value for every fp16 input x <= 0 (checked exhaustively; the
-// library's exp2 self-test entry point re-checks it on the device).
-__device__ __forceinline__ h2_t exp2_h2(h2_t x) { return __builtin_elementwise_exp2(x); }
+// gives 0): v_exp_f16 on the low half, then its SDWA form on the high half,
+// which keeps the low half of the destination.  The SDWA form reads the
+// destination to preserve it, so it must wait for the transcendental result
+// (the s_nop; the compiler does not see this dependency inside the asm).
+// On gfx950 v_exp_f16 returns the correctly rounded value for every fp16
+// input x <= 0 (checked exhaustively; the library's exp2 self-test entry
+// point re-checks this routine on the device).
+__device__ __forceinline__ h2_t exp2_h2(h2_t x) {
+  h2_t y;
+  asm("v_exp_f16 %0, %1\n\ts_nop 1\n\tv_exp_f16_sdwa %0, %1 dst_sel:WORD_1 dst_unused:UNUSED_PRESERVE src0_sel:WORD_1"
+      : "=&v"(y)
+      : "v"(x));
+  return y;
+}
+
+// fp16(a*b) for fp32 a and b, the exact product rounded once (v_fma_mix with
+// an fp16 destination rounds the fused result once; low half of the result).
+__device__ __forceinline__ half_t mul_rn16(float a, float b) {
+  half_t y;
+  asm("v_fma_mixlo_f16 %0, %1, %2, 0" : "=v"(y) : "v"(a), "v"(b));
+  return y;
+}
+
+// Pack fp16(a*c) and fp16(b*c) (each rounded once) into one register.
+__device__ __forceinline__ h2_t mul2_rn16(float a, float b, float c) {
+  h2_t y;
+  asm("v_fma_mixlo_f16 %0, %1, %3, 0\n\tv_fma_mixhi_f16 %0, %2, %3, 0" : "=&v"(y) : "v"(a), "v"(b), "v"(c));
+  return y;
+}
+
+// fp16 nearest to the exact quotient k/s (k an fp16 value, s > 0 fp32): the
+// correctly rounded fp32 quotient rounds to the same fp16 unless it sits
+// exactly on an fp16 midpoint; there the exact remainder k - q*s (exact in
+// fp32 for a correctly rounded q) tells on which side the true quotient lies.
+__device__ __forceinline__ half_t div_rn16(float k, float s) {
+  const float q = k / s;
+  const half_t h = (half_t)q;
+  const float hv = (float)h;
+  if (hv == q) return h;
+  const uint16_t hb = __builtin_bit_cast(uint16_t, h);
+  // neighbour of h on q's side (magnitude up if |q| > |h|)
+  const uint16_t nbb = (fabsf(q) > fabsf(hv)) ? (uint16_t)(hb + 1) : (uint16_t)(hb - 1);
+  const half_t nb = __builtin_bit_cast(half_t, nbb);
+  const float mid = 0.5f * (hv + (float)nb);
+  if (q != mid) return h;
+  const float r = __builtin_fmaf(-q, s, k);        // exact remainder
+  if (r == 0.0f) return h;                          // exact tie: h is the even one
+  const bool above = r > 0.0f;                      // true quotient > q (s > 0)
+  const bool nb_above = (float)nb > q;
+  return (above == nb_above) ? nb : h;
+}
 
 __device__ __forceinline__ float shfl_xor32(float v) {
   return __shfl_xor(v, 32);

@@ -17,9 +17,9 @@ __device__ __forceinline__ int seq_len(const int* cu, int b, int S) {
   return cu ? cu[b + 1] - cu[b] : S;
 }
 
-// Load 32 consecutive fp16 channels of one (token, head) row, apply the
-// Smooth-QK scale (multiply for Q, correctly rounded divide for K, then one
-// rounding to fp16) and return the values as fp32.
+// Load 32 consecutive fp16 channels of one (token, head) row and apply the
+// Smooth-QK scale: q~ = fp16(q*s) and k~ = fp16(k/s), the exact product or
+// quotient rounded once.  Returns the values as fp32.
 template <bool kIsK>
 __device__ __forceinline__ void load_smoothed32(const half_t* __restrict__ src,
                                                 const float* __restrict__ s, float x[32]) {
@@ -33,11 +33,7 @@ __device__ __forceinline__ void load_smoothed32(const half_t* __restrict__ src,
   }
   if (s) {
 #pragma unroll
-    for (int c = 0; c < 32; ++c) {
-      const float sc = s[c];
-      const float y = kIsK ? (x[c] / sc) : (x[c] * sc);
-      x[c] = (float)(half_t)y;
-    }
+    for (int c = 0; c < 32; ++c) x[c] = (float)(kIsK ? div_rn16(x[c], s[c]) : mul_rn16(x[c], s[c]));
   }
 }
 
@@ -156,8 +152,10 @@ __global__ void __launch_bounds__(256) k_quant_v_canon(const half_t* __restrict_
 }
 
 // ---------------------------------------------------------------------------
-// Attention pre-pass (HIF4 operands).  One workgroup per (sequence b, kv
-// head, 64-key block J).  Writes, for the chunk:
+// Attention pre-pass (HIF4 operands).  One workgroup of 4G waves per
+// (sequence b, kv head, 64-key block J); wave w < 2G quantizes K half-tile
+// t = w/G, group g = w%G; wave w >= 2G quantizes V channel tile w-2G.
+// Writes, for the chunk:
 //   K operand [2 halves][G groups][64 lanes][6 dwords]: lane l holds key
 //     32t + l%32 and channels 64g + 32(l/32) + [0,32) in FP6 E2M3, i.e. the
 //     A operand of S^T = K^ Q^T for the 32x32x64 MFMA;
@@ -165,16 +163,21 @@ __global__ void __launch_bounds__(256) k_quant_v_canon(const half_t* __restrict_
 //   V operand [D/32 tiles][64 lanes][6 dwords]: lane l holds channel
 //     32dt + l%32 and, at FP6 slot s, the key 32(s%2) + 8(s/8) + 4(l/32) +
 //     (s/2)%4 -- the key order in which the attention kernel's P^ operand
-//     arrives (see the attention kernel);
-//   V scales  [D] fp32: b/4 of each channel's 64-token group.
+//     arrives;
+//   V scales  [D] uint32: E8M0 bytes that split b/4 = (1 + m/4) 2^(e-33) over
+//     three MFMAs on the same operand: byte0 = 2^(e-33), byte1 = 2^(e-35) if
+//     m&1 else 2^-127, byte2 = 2^(e-34) if m&2 else 2^-127 (2^-127 adds a
+//     contribution below 2^-100 of the others: the output is fp32-accumulated
+//     and only tolerance-checked, unlike the scores).
 __device__ __forceinline__ int v_slot_key(int h, int s) {
   return 32 * (s & 1) + 8 * (s >> 3) + 4 * h + ((s >> 1) & 3);
 }
 
-__global__ void __launch_bounds__(256) k_prep_kv_hif4(const half_t* __restrict__ k, const half_t* __restrict__ v,
-                                                      const float* __restrict__ s, const int* __restrict__ cu,
-                                                      uint8_t* __restrict__ ws, int S, int NB, int heads_kv,
-                                                      int G) {
+__global__ void __launch_bounds__(1024) k_prep_kv_hif4(const half_t* __restrict__ k, const half_t* __restrict__ v,
+                                                       const float* __restrict__ s, const int* __restrict__ cu,
+                                                       uint8_t* __restrict__ ws, int S, int NB, int heads_kv,
+                                                       int G) {
+  extern __shared__ __align__(16) half_t vt[];       // [64 keys][D] tile of V
   const int J = blockIdx.x, hk = blockIdx.y, b = blockIdx.z;
   const int D = 64 * G;
   const int t0 = seq_start(cu, b, S);
@@ -182,64 +185,69 @@ __global__ void __launch_bounds__(256) k_prep_kv_hif4(const half_t* __restrict__
   if (64 * J >= L) return;
   const ChunkLayout lay = chunk_layout_hif4(G);
   uint8_t* chunk = ws + ((size_t)(b * heads_kv + hk) * NB + J) * lay.bytes;
+  // stage V rows [64J, 64J+64) of this head, zero past the sequence end
+  const int n16 = 64 * D / 8;
+  for (int i = threadIdx.x; i < n16; i += blockDim.x) {
+    const int key = i / (D / 8), c8 = i % (D / 8);
+    const int pos = 64 * J + key;
+    uint4 val = make_uint4(0, 0, 0, 0);
+    if (pos < L) val = *reinterpret_cast<const uint4*>(v + ((size_t)(t0 + pos) * heads_kv + hk) * D + 8 * c8);
+    reinterpret_cast<uint4*>(vt)[i] = val;
+  }
+  __syncthreads();
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, h = lane >> 5;
-  const int n_tasks = 2 * G + D / 32;
-  for (int task = wave; task < n_tasks; task += 4) {
-    float x[32], o[32];
-    if (task < 2 * G) {
-      const int t = task / G, g = task % G;
-      const int key = 32 * t + (lane & 31);
-      const int pos = 64 * J + key;
-      if (pos < L) {
-        const half_t* src = k + ((size_t)(t0 + pos) * heads_kv + hk) * D + 64 * g + 32 * h;
-        const float* sp = s ? s + (size_t)hk * D + 64 * g + 32 * h : nullptr;
-        load_smoothed32<true>(src, sp, x);
-      } else {
-#pragma unroll
-        for (int c = 0; c < 32; ++c) x[c] = 0.0f;
-      }
-      const GroupMeta gm = quantize_split<kRows>(x, o, h);
-      h32_t hv;
-#pragma unroll
-      for (int c = 0; c < 32; ++c) hv[c] = (half_t)o[c];
-      const i6_t pk = __builtin_amdgcn_cvt_scalef32_pk32_fp6_f16(hv, 1.0f);
-      int* dst = reinterpret_cast<int*>(chunk + lay.k_op + ((size_t)(t * G + g) * 64 + lane) * 24);
-#pragma unroll
-      for (int i = 0; i < 6; ++i) dst[i] = pk[i];
-      if (h == 0) reinterpret_cast<float*>(chunk + lay.k_scale)[(t * G + g) * 32 + (lane & 31)] = 0.25f * gm.b;
+  float x[32], o[32];
+  if (wave < 2 * G) {
+    const int t = wave / G, g = wave % G;
+    const int key = 32 * t + (lane & 31);
+    const int pos = 64 * J + key;
+    if (pos < L) {
+      const half_t* src = k + ((size_t)(t0 + pos) * heads_kv + hk) * D + 64 * g + 32 * h;
+      const float* sp = s ? s + (size_t)hk * D + 64 * g + 32 * h : nullptr;
+      load_smoothed32<true>(src, sp, x);
     } else {
-      const int dt = task - 2 * G;
-      const int d = 32 * dt + (lane & 31);
 #pragma unroll
-      for (int sl = 0; sl < 32; ++sl) {
-        const int pos = 64 * J + v_slot_key(h, sl);
-        x[sl] = pos < L ? (float)v[((size_t)(t0 + pos) * heads_kv + hk) * D + d] : 0.0f;
-      }
-      // Regroup the slots into the lane's key 4-blocks: block (t, j) holds
-      // keys 32t + 8j + 4h + [0,4), which sit at slots s = 8j + 2i + t.
-      float xb[32], ob[32];
+      for (int c = 0; c < 32; ++c) x[c] = 0.0f;
+    }
+    const GroupMeta gm = quantize_split<kRows>(x, o, h);
+    h32_t hv;
 #pragma unroll
-      for (int kk = 0; kk < 8; ++kk) {
-        const int t = kk >> 2, j = kk & 3;
+    for (int c = 0; c < 32; ++c) hv[c] = (half_t)o[c];
+    const i6_t pk = __builtin_amdgcn_cvt_scalef32_pk32_fp6_f16(hv, 1.0f);
+    int* dst = reinterpret_cast<int*>(chunk + lay.k_op + ((size_t)(t * G + g) * 64 + lane) * 24);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) xb[4 * kk + i] = x[8 * j + 2 * i + t];
-      }
-      // 4-block kk = (t, j) has global index (32t + 8j + 4h)/4 = 8t + 2j + h.
-      const GroupMeta gm = quantize_split<kKeys>(xb, ob, h);
+    for (int i = 0; i < 6; ++i) dst[i] = pk[i];
+    if (h == 0) reinterpret_cast<float*>(chunk + lay.k_scale)[(t * G + g) * 32 + (lane & 31)] = 0.25f * gm.b;
+  } else if (wave < 4 * G) {
+    const int dt = wave - 2 * G;
+    const int d = 32 * dt + (lane & 31);
+    // the lane's key 4-block (t, j) = keys 32t + 8j + 4h + [0,4), held at
+    // slots s = 8j + 2i + t; gather it in block order for the quantizer
 #pragma unroll
-      for (int kk = 0; kk < 8; ++kk) {
-        const int t = kk >> 2, j = kk & 3;
+    for (int kk = 0; kk < 8; ++kk) {
+      const int t = kk >> 2, j = kk & 3;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) o[8 * j + 2 * i + t] = ob[4 * kk + i];
-      }
-      h32_t hv;
+      for (int i = 0; i < 4; ++i) x[4 * kk + i] = (float)vt[(32 * t + 8 * j + 4 * h + i) * D + d];
+    }
+    float ob[32];
+    const GroupMeta gm = quantize_split<kKeys>(x, ob, h);
 #pragma unroll
-      for (int c = 0; c < 32; ++c) hv[c] = (half_t)o[c];
-      const i6_t pk = __builtin_amdgcn_cvt_scalef32_pk32_fp6_f16(hv, 1.0f);
-      int* dst = reinterpret_cast<int*>(chunk + lay.v_op + ((size_t)dt * 64 + lane) * 24);
+    for (int kk = 0; kk < 8; ++kk) {
+      const int t = kk >> 2, j = kk & 3;
 #pragma unroll
-      for (int i = 0; i < 6; ++i) dst[i] = pk[i];
-      if (h == 0) reinterpret_cast<float*>(chunk + lay.v_scale)[d] = 0.25f * gm.b;
+      for (int i = 0; i < 4; ++i) o[8 * j + 2 * i + t] = ob[4 * kk + i];
+    }
+    h32_t hv;
+#pragma unroll
+    for (int c = 0; c < 32; ++c) hv[c] = (half_t)o[c];
+    const i6_t pk = __builtin_amdgcn_cvt_scalef32_pk32_fp6_f16(hv, 1.0f);
+    int* dst = reinterpret_cast<int*>(chunk + lay.v_op + ((size_t)dt * 64 + lane) * 24);
+#pragma unroll
+    for (int i = 0; i < 6; ++i) dst[i] = pk[i];
+    if (h == 0) {
+      const uint32_t e = gm.base >> 2, m = gm.base & 3u;
+      const uint32_t b0 = e + 94u, b1 = (m & 1u) ? e + 92u : 0u, b2 = (m & 2u) ? e + 93u : 0u;
+      reinterpret_cast<uint32_t*>(chunk + lay.v_scale)[d] = b0 | (b1 << 8) | (b2 << 16);
     }
   }
 }
@@ -383,7 +391,8 @@ hipError_t launch_prep_kv(const half_t* k, const half_t* v, const float* s, cons
   if (fp16)
     k_prep_kv_fp16<<<grid, dim3(256), 0, st>>>(k, v, cu, ws, S, NB, heads_kv, D);
   else
-    k_prep_kv_hif4<<<grid, dim3(256), 0, st>>>(k, v, s, cu, ws, S, NB, heads_kv, D / 64);
+    k_prep_kv_hif4<<<grid, dim3(64 * 4 * (D / 64)), 64 * D * sizeof(half_t), st>>>(k, v, s, cu, ws, S, NB, heads_kv,
+                                                                                   D / 64);
   return hipGetLastError();
 }
 

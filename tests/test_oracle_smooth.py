@@ -106,11 +106,45 @@ def test_bypass_and_gate_pick():
     assert s[0, 5] > 1
 
 
-def test_apply_rounding_contract():
-    q = np.ones((1, 1, 64), np.float16)
-    q[..., 1] = 3.0
-    k = q.copy()
-    s = np.full((1, 64), 3.0, np.float32)
-    qt, kt = smooth.apply(q, k, s, 1)
-    assert qt[0, 0, 1] == np.float16(9.0)
-    assert kt[0, 0, 0] == np.float16(np.float32(1.0) / np.float32(3.0))
+def _rn16_exact(fr):
+    """fp16 nearest to a Fraction (ties to even), by exact comparison."""
+    from fractions import Fraction
+    h = np.float16(float(fr))
+    cands = [np.nextafter(h, np.float16(-np.inf)), h, np.nextafter(h, np.float16(np.inf))]
+    best = min(cands, key=lambda c: (abs(Fraction(float(c)) - fr), int(c.view(np.uint16)) & 1))
+    return best
+
+
+def test_apply_single_rounding_exhaustive_sample():
+    """q~ = fp16(q*s) and k~ = fp16(k/s) are the exact product and quotient
+    rounded once; checked with exact rationals on random operands and on
+    operands built so that an fp32 intermediate would sit on an fp16 midpoint
+    (where rounding twice would differ)."""
+    from fractions import Fraction
+    rng = np.random.default_rng(11)
+    q = rng.standard_normal((1, 400, 1, 64)).astype(np.float16)
+    s = np.exp(rng.uniform(-3, 3, (1, 64))).astype(np.float32)
+    qt, kt = smooth.apply(q, q, s, 1)
+    for i in range(0, 400, 7):
+        for c in range(0, 64, 5):
+            fq, fs = Fraction(float(q[0, i, 0, c])), Fraction(float(s[0, c]))
+            assert qt[0, i, 0, c] == _rn16_exact(fq * fs)
+            assert kt[0, i, 0, c] == _rn16_exact(fq / fs)
+    # k/s whose fp32 rounding lands exactly on an fp16 midpoint: s is the fp32
+    # nearest to k/M for a midpoint M, so the fp32 quotient is M itself while
+    # the exact quotient is not
+    found = differ = 0
+    for kv in np.arange(1.0, 2.0, 2.0 ** -6).astype(np.float16):
+        base = np.float16(float(kv) / 1.3)
+        mid = (float(base) + float(np.nextafter(base, np.float16(2)))) / 2
+        sv = np.float32(float(kv) / mid)
+        q32 = np.float32(kv) / sv
+        if float(q32) != mid or Fraction(float(kv)) / Fraction(float(sv)) == Fraction(mid):
+            continue
+        found += 1
+        one = np.full((1, 1, 1, 64), kv, np.float16)
+        got = smooth.apply(one, one, np.full((1, 64), sv, np.float32), 1)[1]
+        want = _rn16_exact(Fraction(float(kv)) / Fraction(float(sv)))
+        assert got[0, 0, 0, 0] == want
+        differ += want != np.float16(q32)   # cases where rounding twice is wrong
+    assert found > 0 and differ > 0
