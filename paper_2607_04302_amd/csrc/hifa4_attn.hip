@@ -12,7 +12,7 @@
 // key blocks first).
 //
 // Per 64-key block (one P group, one V group) and wave:
-//   S^T[key, q] = K^ Q^T with two 32x32x64 FP6 MFMAs per 64-channel group
+//   S^T[key, q] = K^ Q^T with 32x32x64 FP6 MFMAs per 64-channel group
 //     (the A operand is the pre-pass K tile in LDS, B the Q tile quantized in
 //     registers at kernel start); each MFMA sum is exact, the fp32 epilogue
 //     applies b_Q*b_K per group and sums the groups in order, then x c and to
@@ -86,6 +86,12 @@ __device__ __forceinline__ f16v_t mfma6(const i8_t& A, const i8_t& B, const f16v
 
 __device__ __forceinline__ half_t hmax(half_t a, half_t b) { return a > b ? a : b; }
 
+// FP6 x FP6 MFMA whose A rows are scaled by byte OPSEL of `sa` (B unscaled).
+template <int OPSEL>
+__device__ __forceinline__ f16v_t mfma6_rows(const i8_t& A, const i8_t& B, const f16v_t& C, int sa) {
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(A, B, C, 2, 2, OPSEL, sa, 0, 127);
+}
+
 // Lane-pair exchange with v_permlane32_swap(v, v): it swaps the upper 32
 // lanes of the first copy with the lower 32 lanes of the second, so lanes
 // 0..31 see (own, partner) and lanes 32..63 see (partner, own).  Symmetric
@@ -99,7 +105,9 @@ __device__ __forceinline__ Pair32 pair32(uint32_t v) {
 }
 __device__ __forceinline__ h2_t max_with_partner(h2_t v) {
   const Pair32 p = pair32(__builtin_bit_cast(uint32_t, v));
-  return __builtin_elementwise_max(__builtin_bit_cast(h2_t, p.x), __builtin_bit_cast(h2_t, p.y));
+  h2_t y;
+  asm("v_pk_max_f16 %0, %1, %2" : "=v"(y) : "v"(p.x), "v"(p.y));
+  return y;
 }
 __device__ __forceinline__ float add_with_partner(float v) {
   const Pair32 p = pair32(__builtin_bit_cast(uint32_t, v));
@@ -111,14 +119,14 @@ __device__ __forceinline__ h2_t partner_h2(h2_t v, int h) {
   return __builtin_bit_cast(h2_t, h ? p.x : p.y);
 }
 
-// t = fp16(p*R + C) for both halves of p (fp16), R and C fp32: each result is
-// the exact fused value rounded once to fp16.
-__device__ __forceinline__ h2_t fma_grid2(h2_t p, float R, float C) {
+// t = fp16(p*R + C) for both halves of p (fp16), R fp32 and C the low half
+// of c2 (fp16): each result is the exact fused value rounded once to fp16.
+__device__ __forceinline__ h2_t fma_grid2(h2_t p, float R, h2_t c2) {
   h2_t y;
-  asm("v_fma_mixlo_f16 %0, %1, %2, %3 op_sel_hi:[1,0,0]\n\t"
-      "v_fma_mixhi_f16 %0, %1, %2, %3 op_sel:[1,0,0] op_sel_hi:[1,0,0]"
+  asm("v_fma_mixlo_f16 %0, %1, %2, %3 op_sel_hi:[1,0,1]\n\t"
+      "v_fma_mixhi_f16 %0, %1, %2, %3 op_sel:[1,0,0] op_sel_hi:[1,0,1]"
       : "=&v"(y)
-      : "v"(p), "v"(R), "v"(C));
+      : "v"(p), "v"(R), "v"(c2));
   return y;
 }
 
@@ -129,11 +137,20 @@ __device__ __forceinline__ int key_of(int t, int h, int v) { return 32 * t + 8 *
 // ---------------------------------------------------------------------------
 // HiFA4 kernel.
 //
-// Pipeline per wave: the QK^T MFMAs of block J+1 are issued before the
-// softmax / quantization VALU work of block J, so the matrix cores and the
-// vector ALUs overlap.  K/V chunks rotate through three LDS buffers: while
-// block J is consumed (K of J+1, V of J), chunk J+2 is fetched into registers
-// and written to the buffer chunk J-1 used.
+// K/V chunks alternate between two LDS buffers: while block J is consumed,
+// chunk J+1 is fetched into registers and stored to the other buffer before
+// the block's closing barrier.  Two waves per SIMD let one wave's MFMAs run
+// under the other's vector work.  The block that holds a wave's diagonal is
+// processed by a separate instantiation (MASK) so that the causal mask costs
+// nothing on the other blocks.
+//
+// Scores: for each 32-key half t and channel group g two MFMAs accumulate
+// K^'s codes and the second operand of the split base (zero, the codes or the
+// negated codes), with E8M0 row scales that together make K's exact b/4; the
+// result is the exact sum of o_q * (o_k * b_k/4) in fp32.  V^ enters the PV
+// product the same way, so its groups are exact too.  The epilogue
+// multiplies by the lane's own b_q/4 (each lane owns one query in S^T) and adds
+// the groups in order: two VALU operations per score plus the fp16 rounding.
 //
 // Deferred rescale: instead of O <- r*O every block, the kernel keeps
 // O* = O / rho and l* = l / rho with rho the product of the rescale factors so
@@ -141,15 +158,276 @@ __device__ __forceinline__ int key_of(int t, int h, int v) { return 32 * t + 8 *
 // the output and the P^ codes are unchanged; only the fp32 rounding of O
 // differs.  A factor r = 0 (a running max that grows by more than 24 in log2
 // units after the first block) wipes the history, exactly as r*O does.
+
+// fp16 exponential of four packed pairs; the four low-half results are
+// written before the first SDWA high-half instruction reads its destination,
+// which keeps the transcendental result latency out of the way without nops.
+__device__ __forceinline__ void exp2_h2x4(const h2_t x[4], h2_t y[4]) {
+  asm("v_exp_f16 %0, %4\n\t"
+      "v_exp_f16 %1, %5\n\t"
+      "v_exp_f16 %2, %6\n\t"
+      "v_exp_f16 %3, %7\n\t"
+      "v_exp_f16_sdwa %0, %4 dst_sel:WORD_1 dst_unused:UNUSED_PRESERVE src0_sel:WORD_1\n\t"
+      "v_exp_f16_sdwa %1, %5 dst_sel:WORD_1 dst_unused:UNUSED_PRESERVE src0_sel:WORD_1\n\t"
+      "v_exp_f16_sdwa %2, %6 dst_sel:WORD_1 dst_unused:UNUSED_PRESERVE src0_sel:WORD_1\n\t"
+      "v_exp_f16_sdwa %3, %7 dst_sel:WORD_1 dst_unused:UNUSED_PRESERVE src0_sel:WORD_1"
+      : "=&v"(y[0]), "=&v"(y[1]), "=&v"(y[2]), "=&v"(y[3])
+      : "v"(x[0]), "v"(x[1]), "v"(x[2]), "v"(x[3]));
+}
+
+// Packed fp16 max.  Written as an instruction so that the compiler does not
+// canonicalize its (finite or -inf, never NaN) operands first.
+__device__ __forceinline__ h2_t hmax2(h2_t a, h2_t b) {
+  h2_t y;
+  asm("v_pk_max_f16 %0, %1, %2" : "=v"(y) : "v"(a), "v"(b));
+  return y;
+}
+// max of the two halves, in both halves
+__device__ __forceinline__ h2_t hmax_halves(h2_t a) {
+  h2_t y;
+  asm("v_pk_max_f16 %0, %1, %1 op_sel:[0,1] op_sel_hi:[1,0]" : "=v"(y) : "v"(a));
+  return y;
+}
+// (a.lo, b.lo) and (a.hi, b.hi) maxima of two packed pairs: max(a.lo, a.hi),
+// max(b.lo, b.hi) in the low and high halves.
+__device__ __forceinline__ h2_t hmax_pairs(h2_t a, h2_t b) {
+  h2_t y;
+  asm("v_pk_max_f16 %0, %1, %2 op_sel:[0,0] op_sel_hi:[1,1]" : "=v"(y) : "v"(__builtin_shufflevector(a, b, 0, 2)),
+      "v"(__builtin_shufflevector(a, b, 1, 3)));
+  return y;
+}
+
+template <int G>
+struct Hif4State {
+  f16v_t O[2 * G];
+  half_t m_run;
+  float l_star;     // l / rho (consistent or mismatched per NORM)
+  float inv_rho;    // 1 / rho
+};
+
+template <int G, int NORM, bool DEBUG, bool MASK>
+__device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm, const uint8_t* cur, int J, int lane,
+                                           int h, int col, int qi, bool row_ok, const i8_t (&qop)[G],
+                                           const float (&bq)[G], const i8_t& ones, Hif4State<G>& st) {
+  constexpr int DT = 2 * G;
+  constexpr ChunkLayout lay = chunk_layout_hif4(G);
+  // ---- scores: S2 = fp16((sum_g acc_g * b_q/4) * c).
+  h2_t s2[2][8];
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    f16v_t acc[G];
+    int ks[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      ks[g] = reinterpret_cast<const int*>(cur + lay.k_scale)[(t * G + g) * 32 + col];
+      const f16v_t c0 = {};
+      acc[g] = mfma6_rows<0>(ld_op6(cur + lay.k_op + ((size_t)((t * G + g) * 2 + 0) * 64 + lane) * 24), qop[g], c0,
+                             ks[g]);
+    }
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+      acc[g] = mfma6_rows<1>(ld_op6(cur + lay.k_op + ((size_t)((t * G + g) * 2 + 1) * 64 + lane) * 24), qop[g],
+                             acc[g], ks[g]);
+    float sacc[16];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      sacc[v] = acc[0][v] * bq[0];
+#pragma unroll
+      for (int g = 1; g < G; ++g) sacc[v] = __builtin_fmaf(acc[g][v], bq[g], sacc[v]);
+    }
+#pragma unroll
+    for (int v2 = 0; v2 < 8; ++v2) s2[t][v2] = mul2_rn16(sacc[2 * v2], sacc[2 * v2 + 1], a.c);
+  }
+  if (MASK) {
+    const half_t ninf = (half_t)(-__builtin_inff());
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int v = 0; v < 16; ++v)
+        if (64 * J + key_of(t, h, v) > qi) s2[t][v >> 1][v & 1] = ninf;
+  }
+  // ---- running max (FP16), exchanged with lane l^32.
+  h2_t mx2 = hmax2(s2[0][0], s2[1][0]);
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int v2 = 1; v2 < 8; ++v2) mx2 = hmax2(mx2, s2[t][v2]);
+  mx2 = hmax_halves(max_with_partner(mx2));            // block row max, both halves
+  const h2_t mr2 = {st.m_run, st.m_run};
+  const h2_t mn2 = hmax2(mr2, mx2);                    // m_new, both halves
+  // ---- P = 2^(S2 - m_new); r = 2^(m - m_new) and the block max A = 2^(mx - m_new).
+  h2_t p2[2][8];
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      h2_t xin[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) xin[i] = s2[t][4 * q + i] - mn2;
+      exp2_h2x4(xin, &p2[t][4 * q]);
+    }
+  const h2_t ra = exp2_h2(h2_t{mr2[0], mx2[0]} - mn2);
+  const float r = (float)ra[0];
+  const float A = (float)ra[1];
+  st.m_run = mn2[0];
+
+  float psum = 0.0f;
+  if (NORM == 1) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int v2 = 0; v2 < 8; ++v2) psum = __builtin_amdgcn_fdot2(p2[t][v2], h2_t{(half_t)1, (half_t)1}, psum, false);
+    psum = add_with_partner(psum);
+  }
+
+  // ---- P^ = HIF4(P) over the block's 64 keys (P-Reordering).
+  // The lane's 4-block (t, j) holds keys 32t + 8j + 4h + [0,4), i.e. the
+  // packed registers p2[t][2j] and p2[t][2j+1].  Maxima are packed in pairs
+  // of 4-blocks: a4[t][jp] = (A4(t, 2jp), A4(t, 2jp+1)).
+  const uint32_t base = e6m2_ceil(A);
+  const float bval = e6m2_value(base);
+  const float R = hif4_rcp_step(base);
+  // fp16 floors of the half and quarter ranges: an fp16 value x satisfies
+  // x <= 0.875b iff x <= floor16(0.875b) (round-toward-zero conversion).
+  const h2_t thr = __builtin_bit_cast(h2_t, __builtin_amdgcn_cvt_pkrtz(0.875f * bval, 0.4375f * bval));
+  const h2_t th_h = {thr[0], thr[0]}, th_q = {thr[1], thr[1]};
+  // Per 4-block: sh = [a4 <= h] + [a8 <= h and a4 <= q] = 2 - g4h - max(g8h, g4q)
+  // with g = [x > threshold] in {0,1}; non-negative fp16 values order like
+  // their bit patterns, so the tests are saturating 16-bit subtractions.
+  // The rounding constant C16 = 1.5*2^(10-sh) has bits 0x5E00 + (2-sh)<<10.
+  typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
+  const u16x2 uh = __builtin_bit_cast(u16x2, th_h), uq = __builtin_bit_cast(u16x2, th_q);
+  const u16x2 one2 = {1, 1};
+  h2_t cst[2][2];       // rounding constants of 4-blocks (t, 2jp), (t, 2jp+1)
+  h2_t a4s[2][2];
+  uint32_t e2bits = 0, e3bits = 0;
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int jp = 0; jp < 2; ++jp) {
+      const h2_t m0 = hmax2(p2[t][4 * jp], p2[t][4 * jp + 1]);       // 4-block 2jp, two partial maxima
+      const h2_t m1 = hmax2(p2[t][4 * jp + 2], p2[t][4 * jp + 3]);   // 4-block 2jp+1
+      const h2_t a4 = hmax_pairs(m0, m1);
+      const h2_t a8 = max_with_partner(a4);
+      const u16x2 u4 = __builtin_bit_cast(u16x2, a4), u8 = __builtin_bit_cast(u16x2, a8);
+      const u16x2 g4h = __builtin_elementwise_min(__builtin_elementwise_sub_sat(u4, uh), one2);
+      const u16x2 gx = __builtin_elementwise_min(
+          __builtin_elementwise_max(__builtin_elementwise_sub_sat(u8, uh), __builtin_elementwise_sub_sat(u4, uq)), one2);
+      const u16x2 cb = (u16x2){0x5E00, 0x5E00} + ((g4h + gx) << (u16x2){10, 10});
+      cst[t][jp] = __builtin_bit_cast(h2_t, cb);
+      a4s[t][jp] = a4;
+      if (DEBUG) {
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const int j = 2 * jp + e;
+          const bool e2 = a8[e] <= th_h[e];
+          const bool e3 = a4[e] <= (e2 ? th_q[e] : th_h[e]);
+          e2bits |= (uint32_t)e2 << (4 * t + j);
+          e3bits |= (uint32_t)e3 << (8 * t + 2 * j + h);
+          const bool e3o = partner_h2(a4, h)[e] <= (e2 ? th_q[e] : th_h[e]);
+          e3bits |= (uint32_t)e3o << (8 * t + 2 * j + (h ^ 1));
+        }
+      }
+    }
+  // o = u * 2^-sh: one fp16 fma rounds P*R onto the grid 2^-sh, a packed
+  // subtraction removes the offset (both exact).  B-operand slot s holds
+  // tile s/16, register s%16, i.e. the packed registers in order.
+  h32_t ov;
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int v2 = 0; v2 < 8; ++v2) {
+      // 4-block j = v2/2 of tile t: constant in half (j & 1) of cst[t][j >> 1]
+      const h2_t cp = cst[t][v2 >> 2];
+      const h2_t c2 = ((v2 >> 1) & 1) ? __builtin_shufflevector(cp, cp, 1, 1) : __builtin_shufflevector(cp, cp, 0, 0);
+      const h2_t tt = fma_grid2(p2[t][v2], R, c2) - c2;
+      ov[16 * t + 2 * v2] = tt[0];
+      ov[16 * t + 2 * v2 + 1] = tt[1];
+    }
+  const i6_t pk = __builtin_amdgcn_cvt_scalef32_pk32_fp6_f16(ov, 1.0f);
+  i8_t pop;
+#pragma unroll
+  for (int i = 0; i < 6; ++i) pop[i] = pk[i];
+  pop[6] = 0;
+  pop[7] = 0;
+
+  if (DEBUG && row_ok) {
+    uint8_t* dc = a.dbg_codes + (((size_t)tm.hq * a.total_tokens + tm.t0 + qi) * a.NB + J) * 32;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int q4 = 8 * t + 2 * j + h;
+        const int sh = (int)((e2bits >> (4 * t + j)) & 1u) + (int)((e3bits >> q4) & 1u);
+        uint32_t nib[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) nib[i] = (uint32_t)((float)ov[16 * t + 4 * j + i] * (float)(1 << sh));
+        dc[16 * t + 4 * j + 2 * h] = (uint8_t)(nib[0] | (nib[1] << 4));
+        dc[16 * t + 4 * j + 2 * h + 1] = (uint8_t)(nib[2] | (nib[3] << 4));
+      }
+    if (h == 0)
+      a.dbg_meta[((size_t)tm.hq * a.total_tokens + tm.t0 + qi) * a.NB + J] = base | (e2bits << 8) | (e3bits << 16);
+  }
+
+  // ---- deferred rescale bookkeeping (lane-uniform factors).
+  if (__builtin_expect(J > 0 && __builtin_amdgcn_ballot_w64(r == 0.0f) != 0, 0)) {
+    // history wiped for some rows: O <- 0*O, l <- 0*l there
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) st.O[dt][v] = r == 0.0f ? 0.0f : st.O[dt][v];
+    st.l_star = r == 0.0f ? 0.0f : st.l_star;
+  }
+  st.inv_rho = (r == 0.0f) ? 1.0f : st.inv_rho * __builtin_amdgcn_rcpf(r);
+  if (__builtin_expect(__builtin_amdgcn_ballot_w64(st.inv_rho > 0x1p64f) != 0, 0)) {
+    const float rho = __builtin_amdgcn_rcpf(st.inv_rho);
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) st.O[dt][v] *= rho;
+    st.l_star *= rho;
+    st.inv_rho = 1.0f;
+  }
+  const float wp = 0.25f * bval * st.inv_rho;      // b_P/4 / rho
+  // ---- [O | l] += P^ [V^ | 1]; each V^ group enters two MFMAs (split base),
+  // two 32-channel tiles at a time so that consecutive MFMAs are independent.
+#pragma unroll
+  for (int dp = 0; dp < DT; dp += 2) {
+    f16v_t pv[2];
+    int vs[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      vs[i] = reinterpret_cast<const int*>(cur + lay.v_scale)[32 * (dp + i) + col];
+      const f16v_t c0 = {};
+      pv[i] = mfma6_rows<0>(ld_op6(cur + lay.v_op + ((size_t)((dp + i) * 2 + 0) * 64 + lane) * 24), pop, c0, vs[i]);
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      pv[i] = mfma6_rows<1>(ld_op6(cur + lay.v_op + ((size_t)((dp + i) * 2 + 1) * 64 + lane) * 24), pop, pv[i],
+                            vs[i]);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) st.O[dp + i][v] = __builtin_fmaf(pv[i][v], wp, st.O[dp + i][v]);
+  }
+  if (NORM == 1) {
+    st.l_star = __builtin_fmaf(psum, st.inv_rho, st.l_star);
+  } else {
+    const f16v_t zero = {};
+    const f16v_t lacc = mfma6(ones, pop, zero);
+    st.l_star = __builtin_fmaf(lacc[0], wp, st.l_star);
+  }
+}
+
 template <int G, int NORM, bool DEBUG>
-__global__ void __launch_bounds__(256, (G == 1 ? 2 : 1)) k_attn_hif4(AttnArgs a, int heads_per_wg, int qsub, int n_qtiles) {
+__global__ void __launch_bounds__(256, (G <= 2 ? 2 : 1)) k_attn_hif4(AttnArgs a, int heads_per_wg, int qsub,
+                                                                      int n_qtiles) {
   constexpr int D = 64 * G;
   constexpr int DT = D / 32;
   constexpr ChunkLayout lay = chunk_layout_hif4(G);
   constexpr int cbytes = (int)lay.bytes;
   constexpr int n16 = cbytes / 16;
   constexpr int n_pre = (n16 + 255) / 256;
-  constexpr bool kPipe = G <= 2;
   extern __shared__ __align__(16) uint8_t smem[];
   const TileMap tm = map_tile(a, heads_per_wg, qsub, n_qtiles);
   if (!tm.wg_live) return;
@@ -229,242 +507,37 @@ __global__ void __launch_bounds__(256, (G == 1 ? 2 : 1)) k_attn_hif4(AttnArgs a,
     ones[7] = 0;
   }
 
-  f16v_t O[DT];
+  Hif4State<G> st;
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) O[dt][v] = 0.0f;
-  half_t m_run = (half_t)(-__builtin_inff());
-  float l_star = 0.0f;     // l / rho (consistent or mismatched per NORM)
-  float inv_rho = 1.0f;    // 1 / rho
+    for (int v = 0; v < 16; ++v) st.O[dt][v] = 0.0f;
+  st.m_run = (half_t)(-__builtin_inff());
+  st.l_star = 0.0f;
+  st.inv_rho = 1.0f;
 
   const uint8_t* ws_base = a.ws + ((size_t)(tm.b * a.hkv + tm.hk) * a.NB) * lay.bytes;
   stage_chunk(smem, ws_base, cbytes);
-  if (tm.nJ > 1) stage_chunk(smem + cbytes, ws_base + cbytes, cbytes);
   __syncthreads();
 
-  // QK MFMAs of one block: acc[t][g] = K^ tile (t, g) x Q^ group g.
-  f16v_t acc[2][G];
-  auto issue_qk = [&](const uint8_t* buf) {
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        const i8_t kop = ld_op6(buf + lay.k_op + ((size_t)(t * G + g) * 64 + lane) * 24);
-        const f16v_t zero = {};
-        acc[t][g] = mfma6(kop, qop[g], zero);
-      }
-  };
-  if (kPipe && tm.active) issue_qk(smem);
-
   for (int J = 0; J < tm.nJ; ++J) {
-    const uint8_t* cur = smem + (J % 3) * cbytes;
-    const bool has_next2 = J + 2 < tm.nJ;
+    const uint8_t* cur = smem + (J & 1) * cbytes;
+    const bool has_next = J + 1 < tm.nJ;
     u4_t pre[n_pre];
     {
-      const u4_t* src = reinterpret_cast<const u4_t*>(ws_base + (size_t)(has_next2 ? J + 2 : J) * cbytes);
+      const u4_t* src = reinterpret_cast<const u4_t*>(ws_base + (size_t)(has_next ? J + 1 : J) * cbytes);
 #pragma unroll
       for (int r = 0; r < n_pre; ++r) {
         const int i = threadIdx.x + 256 * r;
         pre[r] = src[i < n16 ? i : n16 - 1];
       }
     }
-    if (tm.active && J <= jw_last) {
-      if (!kPipe) issue_qk(cur);
-      // ---- scores: S2 = fp16((sum_g t_g) * c), t_g = acc_g * (b_q b_k) exact.
-      h2_t s2[2][8];
-#pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        float sacc[16];
-#pragma unroll
-        for (int g = 0; g < G; ++g) {
-          const float* ksc = reinterpret_cast<const float*>(cur + lay.k_scale) + (t * G + g) * 32 + 4 * h;
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const f4_t bkv = *reinterpret_cast<const f4_t*>(ksc + 8 * j);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const int v = 4 * j + i;
-              const float w = bq[g] * bkv[i];
-              sacc[v] = (g == 0) ? acc[t][g][v] * w : __builtin_fmaf(acc[t][g][v], w, sacc[v]);
-            }
-          }
-        }
-#pragma unroll
-        for (int v2 = 0; v2 < 8; ++v2) s2[t][v2] = mul2_rn16(sacc[2 * v2], sacc[2 * v2 + 1], a.c);
-      }
-      // ---- issue the next block's QK^T while this block's VALU work runs.
-      if (kPipe && J < jw_last) issue_qk(smem + ((J + 1) % 3) * cbytes);
-      // ---- causal mask on the block that holds the diagonal.
-      if (J == jw_last) {
-        const half_t ninf = (half_t)(-__builtin_inff());
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-          for (int v = 0; v < 16; ++v)
-            if (64 * J + key_of(t, h, v) > qi) s2[t][v >> 1][v & 1] = ninf;
-      }
-      // ---- running max (FP16), exchanged with lane l^32.
-      h2_t mx2 = s2[0][0];
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int v2 = 0; v2 < 8; ++v2) mx2 = __builtin_elementwise_max(mx2, s2[t][v2]);
-      mx2 = max_with_partner(mx2);
-      const half_t mx = hmax(mx2[0], mx2[1]);
-      const half_t m_new = hmax(m_run, mx);
-      const h2_t mn2 = {m_new, m_new};
-      // ---- P = 2^(S2 - m_new), r = 2^(m - m_new), block max A = 2^(mx - m_new).
-      h2_t p2[2][8];
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int v2 = 0; v2 < 8; ++v2) p2[t][v2] = exp2_h2(s2[t][v2] - mn2);
-      const h2_t ra = exp2_h2(h2_t{(half_t)(m_run - m_new), (half_t)(mx - m_new)});
-      const float r = (float)ra[0];
-      const float A = (float)ra[1];
-      m_run = m_new;
-
-      float psum = 0.0f;
-      if (NORM == 1) {
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-          for (int v2 = 0; v2 < 8; ++v2) psum = __builtin_amdgcn_fdot2(p2[t][v2], h2_t{(half_t)1, (half_t)1}, psum, false);
-        psum = add_with_partner(psum);
-      }
-
-      // ---- P^ = HIF4(P) over the block's 64 keys (P-Reordering).
-      // Lane 4-block (t, j): keys 32t + 8j + 4h + [0,4) = p2[t][2j], p2[t][2j+1].
-      h2_t a4p[4];          // own 4-block maxima, packed (t,0|t,1), (t,2|t,3)
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int jp = 0; jp < 2; ++jp) {
-          const h2_t m0 = __builtin_elementwise_max(p2[t][4 * jp], p2[t][4 * jp + 1]);
-          const h2_t m1 = __builtin_elementwise_max(p2[t][4 * jp + 2], p2[t][4 * jp + 3]);
-          a4p[2 * t + jp] = h2_t{hmax(m0[0], m0[1]), hmax(m1[0], m1[1])};
-        }
-      const uint32_t base = e6m2_ceil(A);
-      const float bval = e6m2_value(base);
-      const float R = hif4_rcp_step(base);
-      // fp16 floors of the half and quarter ranges: an fp16 value x satisfies
-      // x <= 0.875b iff x <= floor16(0.875b) (round-toward-zero conversion).
-      const h2_t thr = __builtin_bit_cast(h2_t, __builtin_amdgcn_cvt_pkrtz(0.875f * bval, 0.4375f * bval));
-      uint32_t e2bits = 0, e3bits = 0;
-      h2_t cpair[8];        // per 4-block rounding constant (fp16, both halves)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const h2_t a8 = max_with_partner(a4p[q]);
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-          const int t = q >> 1, j = 2 * (q & 1) + e;
-          const bool e2 = a8[e] <= thr[0];
-          const bool e3 = a4p[q][e] <= (e2 ? thr[1] : thr[0]);
-          const int sh = (int)e2 + (int)e3;
-          // C16 = 1.5 * 2^(10-sh) as fp16: exponent field 25 - sh, mantissa 0x200
-          const uint16_t cb = (uint16_t)(((25 - sh) << 10) | 0x200);
-          const half_t c16 = __builtin_bit_cast(half_t, cb);
-          cpair[4 * t + j] = h2_t{c16, c16};
-          if (DEBUG) {
-            e2bits |= (uint32_t)e2 << (4 * t + j);
-            e3bits |= (uint32_t)e3 << (8 * t + 2 * j + h);
-            const bool e3o = partner_h2(a4p[q], h)[e] <= (e2 ? thr[1] : thr[0]);
-            e3bits |= (uint32_t)e3o << (8 * t + 2 * j + (h ^ 1));
-          }
-        }
-      }
-      // o = u * 2^-sh: round P*R onto the grid 2^-sh in one fp16 fma, then
-      // subtract the offset (both exact); then pack 32 values to FP6.
-      h32_t ov;
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const h2_t c2 = cpair[4 * t + j];
-#pragma unroll
-          for (int e = 0; e < 2; ++e) {
-            const h2_t pv = p2[t][2 * j + e];
-            h2_t tt = fma_grid2(pv, R, (float)c2[0]);
-            tt = tt - c2;
-            // slot order of the B operand: slot 2v + t holds tile t, reg v
-            const int v0 = 4 * j + 2 * e;
-            ov[2 * v0 + t] = tt[0];
-            ov[2 * (v0 + 1) + t] = tt[1];
-          }
-        }
-      const i6_t pk = __builtin_amdgcn_cvt_scalef32_pk32_fp6_f16(ov, 1.0f);
-      i8_t pop;
-#pragma unroll
-      for (int i = 0; i < 6; ++i) pop[i] = pk[i];
-      pop[6] = 0;
-      pop[7] = 0;
-
-      if (DEBUG && row_ok) {
-        uint8_t* dc = a.dbg_codes + (((size_t)tm.hq * a.total_tokens + tm.t0 + qi) * a.NB + J) * 32;
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int q4 = 8 * t + 2 * j + h;
-            const int sh = (int)((e2bits >> (4 * t + j)) & 1u) + (int)((e3bits >> q4) & 1u);
-            uint32_t nib[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const int v = 4 * j + i;
-              nib[i] = (uint32_t)((float)ov[2 * v + t] * (float)(1 << sh));
-            }
-            dc[16 * t + 4 * j + 2 * h] = (uint8_t)(nib[0] | (nib[1] << 4));
-            dc[16 * t + 4 * j + 2 * h + 1] = (uint8_t)(nib[2] | (nib[3] << 4));
-          }
-        if (h == 0)
-          a.dbg_meta[((size_t)tm.hq * a.total_tokens + tm.t0 + qi) * a.NB + J] = base | (e2bits << 8) | (e3bits << 16);
-      }
-
-      // ---- deferred rescale bookkeeping (lane-uniform factors).
-      if (J > 0 && __builtin_amdgcn_ballot_w64(r == 0.0f) != 0) {
-        // history wiped for some rows: O <- 0*O, l <- 0*l there
-        if (r == 0.0f) {
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) O[dt][v] = 0.0f;
-          l_star = 0.0f;
-        }
-      }
-      inv_rho = (r == 0.0f) ? 1.0f : inv_rho * __builtin_amdgcn_rcpf(r);
-      if (__builtin_amdgcn_ballot_w64(inv_rho > 0x1p64f) != 0) {
-        const float rho = __builtin_amdgcn_rcpf(inv_rho);
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) O[dt][v] *= rho;
-        l_star *= rho;
-        inv_rho = 1.0f;
-      }
-      const float wp = 0.25f * bval * inv_rho;      // b_P/4 / rho
-      // ---- [O | l] += P^ [V^ | 1]; V^'s scale is split over three MFMAs.
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const i8_t vop = ld_op6(cur + lay.v_op + ((size_t)dt * 64 + lane) * 24);
-        const int vs = reinterpret_cast<const int*>(cur + lay.v_scale)[32 * dt + col];
-        f16v_t pv = {};
-        pv = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vop, pop, pv, 2, 2, 0, vs, 0, 127);
-        pv = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vop, pop, pv, 2, 2, 1, vs, 0, 127);
-        pv = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vop, pop, pv, 2, 2, 2, vs, 0, 127);
-#pragma unroll
-        for (int v = 0; v < 16; ++v) O[dt][v] = __builtin_fmaf(pv[v], wp, O[dt][v]);
-      }
-      if (NORM == 1) {
-        l_star = __builtin_fmaf(psum, inv_rho, l_star);
-      } else {
-        const f16v_t zero = {};
-        const f16v_t lacc = mfma6(ones, pop, zero);
-        l_star = __builtin_fmaf(lacc[0], wp, l_star);
-      }
-    }
-    if (has_next2) {
-      u4_t* dst = reinterpret_cast<u4_t*>(smem + ((J + 2) % 3) * cbytes);
+    if (J < jw_last)
+      hif4_block<G, NORM, DEBUG, false>(a, tm, cur, J, lane, h, col, qi, row_ok, qop, bq, ones, st);
+    else if (J == jw_last)
+      hif4_block<G, NORM, DEBUG, true>(a, tm, cur, J, lane, h, col, qi, row_ok, qop, bq, ones, st);
+    if (has_next) {
+      u4_t* dst = reinterpret_cast<u4_t*>(smem + ((J + 1) & 1) * cbytes);
 #pragma unroll
       for (int r = 0; r < n_pre; ++r) {
         const int i = threadIdx.x + 256 * r;
@@ -476,7 +549,7 @@ __global__ void __launch_bounds__(256, (G == 1 ? 2 : 1)) k_attn_hif4(AttnArgs a,
 
   // ---- finalize: O = fp16(O*/l*), LSE = m ln2 + ln(l* rho).
   if (row_ok) {
-    const float inv = 1.0f / l_star;
+    const float inv = 1.0f / st.l_star;
     half_t* dst = a.o + ((size_t)(tm.t0 + qi) * a.hq + tm.hq) * D;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
@@ -485,12 +558,12 @@ __global__ void __launch_bounds__(256, (G == 1 ? 2 : 1)) k_attn_hif4(AttnArgs a,
         typedef _Float16 h4_t __attribute__((ext_vector_type(4)));
         h4_t o4;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) o4[i] = (half_t)(O[dt][4 * j + i] * inv);
+        for (int i = 0; i < 4; ++i) o4[i] = (half_t)(st.O[dt][4 * j + i] * inv);
         *reinterpret_cast<h4_t*>(dst + 32 * dt + 8 * j + 4 * h) = o4;
       }
     if (h == 0)
       a.lse[(size_t)tm.hq * a.total_tokens + tm.t0 + qi] =
-          (float)m_run * 0.69314718055994531f + logf(l_star) - logf(inv_rho);
+          (float)st.m_run * 0.69314718055994531f + logf(st.l_star) - logf(st.inv_rho);
   }
 }
 
@@ -655,7 +728,7 @@ hipError_t launch_attention(const AttnArgs& a, int norm, bool fp16, hipStream_t 
     }
     return hipErrorInvalidValue;
   }
-  const size_t lds = 3 * chunk_layout_hif4(a.D / 64).bytes;
+  const size_t lds = 2 * chunk_layout_hif4(a.D / 64).bytes;
   const bool dbg = a.dbg_codes != nullptr;
 #define HIFA4_DISPATCH(G)                                                                            \
   do {                                                                                               \

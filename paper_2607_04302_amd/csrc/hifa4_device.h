@@ -34,45 +34,50 @@ typedef int i8_t __attribute__((ext_vector_type(8)));
 // in 6-bit fields: the all-ones operand of the fused normalizer [V^ | 1].
 constexpr uint32_t kE2M3One = 0x08;
 
-// E6M2 value of a base byte: (1 + m/4) * 2^(e - 31).
-__device__ __forceinline__ float e6m2_value(uint32_t code) {
-  return __builtin_ldexpf(1.0f + 0.25f * (float)(code & 3u), (int)(code >> 2) - 31);
-}
 
 // Smallest E6M2 byte whose value b satisfies 1.75*b >= A (A >= 0, an fp16 or
-// fp16-softmax value held exactly in fp32).  A first guess comes from
-// A*(4/7) rounded up to two mantissa bits; the two exact comparisons below
-// (1.75*b is exact in fp32) correct the at most one-step error of the guess.
+// fp16-softmax value held exactly in fp32), without branches.  Write
+// A = s*2^E with s in [1,2).  The values 1.75*b of the bases near A are
+// 1.09375, 1.3125, 1.53125 (mantissas m = 1, 2, 3, exponent E-1), 1.75 and
+// 2.1875 (m = 0, 1, exponent E) times 2^E, so the smallest covering base is
+// code 4(E+30) + 1 + [s > 1.09375] + [s > 1.3125] + [s > 1.53125] + [s > 1.75];
+// the comparisons are exact on the fp32 significand bits.  A = 0 gives 0.
 __device__ __forceinline__ uint32_t e6m2_ceil(float A) {
-  if (!(A > 0.0f)) return 0u;
-  const float T = A * (4.0f / 7.0f);
-  const uint32_t bits = __float_as_uint(T);
-  int code = (((int)((bits >> 23) & 255u) - 127 + 31) << 2) | (int)((bits >> 21) & 3u);
-  if (bits & 0x1FFFFFu) code += 1;
-  code = code < 0 ? 0 : (code > 255 ? 255 : code);
-  if (code > 0 && 1.75f * e6m2_value((uint32_t)(code - 1)) >= A) code -= 1;
-  if (code < 255 && 1.75f * e6m2_value((uint32_t)code) < A) code += 1;
-  return (uint32_t)code;
+  const uint32_t bits = __float_as_uint(A);
+  const uint32_t mant = bits & 0x7FFFFFu;
+  const int c = (int)(mant > 0xC0000u) + (int)(mant > 0x280000u) + (int)(mant > 0x440000u) +
+                (int)(mant > 0x600000u);
+  const int code = 4 * (int)(bits >> 23) - 387 + c;
+  return A > 0.0f ? (uint32_t)code : 0u;
+}
+
+// E6M2 value b = (1 + m/4) * 2^(e-31) of byte e<<2|m, built from its bits.
+__device__ __forceinline__ float e6m2_bits_value(uint32_t code) {
+  return __uint_as_float((code << 21) + 0x30000000u);
 }
 
 // R = (4/b) * (1 + 2^-18), rounded: for the 4 base mantissas the constant
-// fp32(16/(4+m) * (1 + 2^-18)), then an exact power-of-two scaling.
+// fp32(16/(4+m) * (1 + 2^-18)), then an exact power-of-two scaling by
+// 2^(31-e) applied to the exponent field.
 //
-// Element rounding uses o = fl(a*R + C_sh) - C_sh with C_sh = 1.5*2^(23-sh):
-// the fused multiply-add rounds the exact product a*R once onto the grid
-// 2^-sh, which is u*2^-sh with u = round-half-to-even(a/step * (1+beta)).
-// a/step is an fp16 value divided by (4+m)*2^k: a non-tie lies at least
-// 2^-12 (relative) from a half-integer while beta ~ 2^-18, so those round as
-// exactly as without beta; an exact tie n+1/2 is pushed strictly above and
-// rounds away from zero.  The result is exactly round-half-away(a/step).
+// Element rounding uses o = fl(a*R + C_sh) - C_sh with C_sh = 1.5*2^(23-sh)
+// (fp32) or 1.5*2^(10-sh) (fp16 destination): the fused multiply-add rounds
+// the exact product a*R once onto the grid 2^-sh, which is u*2^-sh with
+// u = round-half-to-even(a/step * (1+beta)).  a/step is an fp16 value divided
+// by (4+m)*2^k: a non-tie lies at least 2^-12 (relative) from a half-integer
+// while beta ~ 2^-18, so those round as exactly as without beta; an exact tie
+// n+1/2 is pushed strictly above and rounds away from zero.  The result is
+// exactly round-half-away(a/step).
 __device__ __forceinline__ float hif4_rcp_step(uint32_t code) {
   const uint32_t m = code & 3u;
-  const float r = m == 0 ? 0x1.00004p+2f
-                : m == 1 ? 0x1.999ap+1f
-                : m == 2 ? 0x1.5555aap+1f
-                         : 0x1.249292p+1f;
-  return __builtin_ldexpf(r, 31 - (int)(code >> 2));
+  const uint32_t lo = (m & 1u) ? 0x404ccd00u : 0x40800020u;   // m = 1 : 0
+  const uint32_t hi = (m & 1u) ? 0x40124949u : 0x402aaad5u;   // m = 3 : 2
+  const uint32_t cb = (m & 2u) ? hi : lo;
+  return __uint_as_float(cb + (uint32_t)((31 - (int)(code >> 2)) << 23));
 }
+
+// E6M2 value of a base byte: (1 + m/4) * 2^(e - 31).
+__device__ __forceinline__ float e6m2_value(uint32_t code) { return e6m2_bits_value(code); }
 
 __device__ __forceinline__ float round_const(int sh) {
   return sh == 0 ? 12582912.0f : (sh == 1 ? 6291456.0f : 3145728.0f);

@@ -17,14 +17,17 @@ struct ChunkLayout {
 
 __host__ __device__ constexpr size_t round_up256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// HIF4 operands: K [2][G][64][24 B], K scales [2][G][32] fp32,
-// V [D/32][64][24 B], V scales [D] fp32.
+// HIF4 operands, each group as the two MFMA operands of its split base
+// (operand A = codes, B = zero, codes or negated codes; byte 0 / 1 of the
+// scale word are their E8M0 scales):
+//   K [2 halves][G][2 operands][64 lanes][24 B], K scale words [2][G][32 keys],
+//   V [D/32][2 operands][64 lanes][24 B], V scale words [D].
 __host__ __device__ constexpr ChunkLayout chunk_layout_hif4(int G) {
   ChunkLayout c{};
   c.k_op = 0;
-  c.k_scale = round_up256((size_t)2 * G * 64 * 24);
+  c.k_scale = round_up256((size_t)2 * G * 2 * 64 * 24);
   c.v_op = c.k_scale + round_up256((size_t)2 * G * 32 * 4);
-  c.v_scale = c.v_op + round_up256((size_t)(2 * G) * 64 * 24);
+  c.v_scale = c.v_op + round_up256((size_t)(2 * G) * 2 * 64 * 24);
   c.bytes = c.v_scale + round_up256((size_t)64 * G * 4);
   return c;
 }

@@ -156,21 +156,45 @@ __global__ void __launch_bounds__(256) k_quant_v_canon(const half_t* __restrict_
 // (sequence b, kv head, 64-key block J); wave w < 2G quantizes K half-tile
 // t = w/G, group g = w%G; wave w >= 2G quantizes V channel tile w-2G.
 // Writes, for the chunk:
-//   K operand [2 halves][G groups][64 lanes][6 dwords]: lane l holds key
+//   K operands [2 halves][G groups][2][64 lanes][6 dwords]: lane l holds key
 //     32t + l%32 and channels 64g + 32(l/32) + [0,32) in FP6 E2M3, i.e. the
-//     A operand of S^T = K^ Q^T for the 32x32x64 MFMA;
-//   K scales  [2][G][32] fp32: b/4 per key and group;
-//   V operand [D/32 tiles][64 lanes][6 dwords]: lane l holds channel
-//     32dt + l%32 and, at FP6 slot s, the key 32(s%2) + 8(s/8) + 4(l/32) +
-//     (s/2)%4 -- the key order in which the attention kernel's P^ operand
-//     arrives;
-//   V scales  [D] uint32: E8M0 bytes that split b/4 = (1 + m/4) 2^(e-33) over
-//     three MFMAs on the same operand: byte0 = 2^(e-33), byte1 = 2^(e-35) if
-//     m&1 else 2^-127, byte2 = 2^(e-34) if m&2 else 2^-127 (2^-127 adds a
-//     contribution below 2^-100 of the others: the output is fp32-accumulated
-//     and only tolerance-checked, unlike the scores).
-__device__ __forceinline__ int v_slot_key(int h, int s) {
-  return 32 * (s & 1) + 8 * (s >> 3) + 4 * h + ((s >> 1) & 3);
+//     A operand of S^T = K^ Q^T for the 32x32x64 MFMA, as the two operands of
+//     the key's split base (below);
+//   K scale words [2][G][32]: their two E8M0 bytes per key and group;
+//   V operands [D/32 tiles][2][64 lanes][6 dwords]: lane l holds channel
+//     32dt + l%32 and, at FP6 slot s, the key 32(s/16) + 8((s%16)/4) +
+//     4(l/32) + s%4 -- the key order in which the attention kernel's P^
+//     operand arrives (the S^T accumulator registers of both 32-key halves in
+//     order) -- again as the two operands of the split base;
+//   V scale words [D]: their two E8M0 bytes per channel.
+// Two-operand form of a HIF4 group for the FP6 MFMA.  The base
+// b = (1 + m/4) 2^(e-31) is not an E8M0 power of two, so the group's codes
+// enter two MFMAs whose E8M0 scales add up to b/4 exactly:
+//   m = 0:  1    = 1                 operand B all zero
+//   m = 1:  1.25 = 1 + 1/4           B = codes,          scale 2^(e-35)
+//   m = 2:  1.5  = 1 + 1/2           B = codes,          scale 2^(e-34)
+//   m = 3:  1.75 = 2 - 1/4           B = negated codes,  scale 2^(e-35)
+// operand A = codes with scale 2^(e-33), or 2^(e-32) for m = 3.  The E8M0
+// byte of 2^k is k + 127.  Byte 0 of the scale word serves operand A, byte 1
+// operand B.
+__device__ __forceinline__ uint32_t split_scale_word(uint32_t base) {
+  const uint32_t e = base >> 2, m = base & 3u;
+  const uint32_t sa = e + 94u + (m == 3u ? 1u : 0u);
+  const uint32_t sb = e + (m == 2u ? 93u : 92u);
+  return sa | (sb << 8);
+}
+
+// Stores operand A (the lane's 24 code bytes) at dst and operand B 64 lanes
+// (1536 bytes) later.  The E2M3 sign is bit 5 of each 6-bit field.
+__device__ __forceinline__ void store_split_operand(int* dst, const i6_t& pk, uint32_t base) {
+  constexpr uint32_t kSign[3] = {0x20820820u, 0x08208208u, 0x82082082u};   // fields 6s+5, period 96 bits
+  const uint32_t m = base & 3u;
+#pragma unroll
+  for (int i = 0; i < 6; ++i) {
+    const uint32_t w = (uint32_t)pk[i];
+    dst[i] = (int)w;
+    dst[64 * 6 + i] = (int)(m == 0u ? 0u : (m == 3u ? w ^ kSign[i % 3] : w));
+  }
 }
 
 __global__ void __launch_bounds__(1024) k_prep_kv_hif4(const half_t* __restrict__ k, const half_t* __restrict__ v,
@@ -214,41 +238,29 @@ __global__ void __launch_bounds__(1024) k_prep_kv_hif4(const half_t* __restrict_
 #pragma unroll
     for (int c = 0; c < 32; ++c) hv[c] = (half_t)o[c];
     const i6_t pk = __builtin_amdgcn_cvt_scalef32_pk32_fp6_f16(hv, 1.0f);
-    int* dst = reinterpret_cast<int*>(chunk + lay.k_op + ((size_t)(t * G + g) * 64 + lane) * 24);
-#pragma unroll
-    for (int i = 0; i < 6; ++i) dst[i] = pk[i];
-    if (h == 0) reinterpret_cast<float*>(chunk + lay.k_scale)[(t * G + g) * 32 + (lane & 31)] = 0.25f * gm.b;
+    int* dst = reinterpret_cast<int*>(chunk + lay.k_op + ((size_t)(t * G + g) * 2 * 64 + lane) * 24);
+    store_split_operand(dst, pk, gm.base);
+    if (h == 0)
+      reinterpret_cast<uint32_t*>(chunk + lay.k_scale)[(t * G + g) * 32 + (lane & 31)] = split_scale_word(gm.base);
   } else if (wave < 4 * G) {
     const int dt = wave - 2 * G;
     const int d = 32 * dt + (lane & 31);
-    // the lane's key 4-block (t, j) = keys 32t + 8j + 4h + [0,4), held at
-    // slots s = 8j + 2i + t; gather it in block order for the quantizer
+    // slot s = 4kk + i holds key 32t + 8j + 4h + i of the lane's 4-block
+    // kk = (t, j), which is the quantizer's block order as well
 #pragma unroll
     for (int kk = 0; kk < 8; ++kk) {
       const int t = kk >> 2, j = kk & 3;
 #pragma unroll
       for (int i = 0; i < 4; ++i) x[4 * kk + i] = (float)vt[(32 * t + 8 * j + 4 * h + i) * D + d];
     }
-    float ob[32];
-    const GroupMeta gm = quantize_split<kKeys>(x, ob, h);
-#pragma unroll
-    for (int kk = 0; kk < 8; ++kk) {
-      const int t = kk >> 2, j = kk & 3;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) o[8 * j + 2 * i + t] = ob[4 * kk + i];
-    }
+    const GroupMeta gm = quantize_split<kKeys>(x, o, h);
     h32_t hv;
 #pragma unroll
     for (int c = 0; c < 32; ++c) hv[c] = (half_t)o[c];
     const i6_t pk = __builtin_amdgcn_cvt_scalef32_pk32_fp6_f16(hv, 1.0f);
-    int* dst = reinterpret_cast<int*>(chunk + lay.v_op + ((size_t)dt * 64 + lane) * 24);
-#pragma unroll
-    for (int i = 0; i < 6; ++i) dst[i] = pk[i];
-    if (h == 0) {
-      const uint32_t e = gm.base >> 2, m = gm.base & 3u;
-      const uint32_t b0 = e + 94u, b1 = (m & 1u) ? e + 92u : 0u, b2 = (m & 2u) ? e + 93u : 0u;
-      reinterpret_cast<uint32_t*>(chunk + lay.v_scale)[d] = b0 | (b1 << 8) | (b2 << 16);
-    }
+    int* dst = reinterpret_cast<int*>(chunk + lay.v_op + ((size_t)dt * 2 * 64 + lane) * 24);
+    store_split_operand(dst, pk, gm.base);
+    if (h == 0) reinterpret_cast<uint32_t*>(chunk + lay.v_scale)[d] = split_scale_word(gm.base);
   }
 }
 

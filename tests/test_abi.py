@@ -64,8 +64,9 @@ def test_workspace_sizes(lib):
     p = _p(max_seqlen=4096, num_heads_q=32, num_heads_kv=8)
     o = h.FwdOptions(0, 0, 0, None, None, None)
     n = lib.hifa4_workspace_bytes(ctypes.byref(p), ctypes.byref(o))
-    # 64 blocks x 8 kv heads x (6 KB K op + 512 B scales + 6 KB V op + 512 B)
-    assert n == 64 * 8 * 13312
+    # 64 blocks x 8 kv heads x (3 x 6 KB K operand variants + 512 B K scale
+    # words + 6 KB V operand + 512 B V scale words)
+    assert n == 64 * 8 * 25600
     o16 = h.FwdOptions(0, 1, 0, None, None, None)
     assert lib.hifa4_workspace_bytes(ctypes.byref(p), ctypes.byref(o16)) == 64 * 8 * 32768
     assert lib.hifa4_workspace_bytes(ctypes.byref(_p(head_dim=80)), ctypes.byref(o)) == 0
