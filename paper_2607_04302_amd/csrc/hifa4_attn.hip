@@ -70,11 +70,39 @@ __device__ __forceinline__ void stage_chunk(uint8_t* lds, const uint8_t* __restr
   for (int i = threadIdx.x; i < bytes / 16; i += blockDim.x) dst[i] = src[i];
 }
 
-__device__ __forceinline__ i8_t ld_op6(const uint8_t* p) {
-  const uint2* q = reinterpret_cast<const uint2*>(p);
-  const uint2 a = q[0], b = q[1], c = q[2];
+// Start an asynchronous copy of one chunk (BYTES, a multiple of 16) from
+// global memory straight into LDS (global_load_lds, 16 bytes per lane; lane i
+// of a wave lands at the wave's LDS base + 16 i).  Completion is tracked by
+// vmcnt: the caller waits with vmcnt(0) and a barrier before reading.
+template <int BYTES>
+__device__ __forceinline__ void stage_chunk_async(uint8_t* lds, const uint8_t* __restrict__ g) {
+  constexpr int n16 = BYTES / 16;
+  const int wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int r = 0; r < (n16 + 255) / 256; ++r) {
+    const int i = threadIdx.x + 256 * r;
+    if (256 * r + 64 * wave < n16)          // whole waves: n16 is a multiple of 64
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(g + 16 * (size_t)i),
+                                       (__attribute__((address_space(3))) void*)(lds + 4096 * r + 1024 * wave), 16,
+                                       0, 0);
+  }
+}
+
+__device__ __forceinline__ void wait_async_copies() { __builtin_amdgcn_s_waitcnt(0x0F70); }   // vmcnt(0)
+
+// One lane's 24-byte FP6 operand from an operand record (64 lanes x 16
+// bytes, then 64 lanes x 8 bytes).  The 8-byte tail is read through a volatile
+// access so that the compiler does not pair it with the tail of another
+// operand into one 16-byte read, which would cost register copies to rebuild
+// the contiguous 6-register MFMA operand.
+__device__ __forceinline__ i8_t ld_op6(const uint8_t* rec, int lane) {
+  typedef uint32_t u2_t __attribute__((ext_vector_type(2)));
+  typedef uint32_t u4v_t __attribute__((ext_vector_type(4)));
+  typedef const volatile __attribute__((address_space(3))) u2_t lds_u2_t;
+  const u4v_t a = *reinterpret_cast<const u4v_t*>(rec + 16 * lane);
+  const u2_t c = *(lds_u2_t*)(rec + 1024 + 8 * lane);
   i8_t r;
-  r[0] = (int)a.x; r[1] = (int)a.y; r[2] = (int)b.x; r[3] = (int)b.y; r[4] = (int)c.x; r[5] = (int)c.y;
+  r[0] = (int)a.x; r[1] = (int)a.y; r[2] = (int)a.z; r[3] = (int)a.w; r[4] = (int)c.x; r[5] = (int)c.y;
   r[6] = 0; r[7] = 0;
   return r;
 }
@@ -119,15 +147,48 @@ __device__ __forceinline__ h2_t partner_h2(h2_t v, int h) {
   return __builtin_bit_cast(h2_t, h ? p.x : p.y);
 }
 
-// t = fp16(p*R + C) for both halves of p (fp16), R fp32 and C the low half
-// of c2 (fp16): each result is the exact fused value rounded once to fp16.
-__device__ __forceinline__ h2_t fma_grid2(h2_t p, float R, h2_t c2) {
+// o = fp16(p*R + C) - C for both halves of p (fp16), R fp32 and C half SEL
+// of cp (fp16).  The fused value is rounded once to fp16, onto the grid of C;
+// the subtraction is exact.
+template <int SEL>
+__device__ __forceinline__ h2_t grid_round2(h2_t p, float R, h2_t cp) {
   h2_t y;
-  asm("v_fma_mixlo_f16 %0, %1, %2, %3 op_sel_hi:[1,0,1]\n\t"
-      "v_fma_mixhi_f16 %0, %1, %2, %3 op_sel:[1,0,0] op_sel_hi:[1,0,1]"
-      : "=&v"(y)
-      : "v"(p), "v"(R), "v"(c2));
+  if (SEL == 0)
+    asm("v_fma_mixlo_f16 %0, %1, %2, %3 op_sel:[0,0,0] op_sel_hi:[1,0,1]\n\t"
+        "v_fma_mixhi_f16 %0, %1, %2, %3 op_sel:[1,0,0] op_sel_hi:[1,0,1]\n\t"
+        "v_pk_add_f16 %0, %0, %3 op_sel:[0,0] op_sel_hi:[1,0] neg_lo:[0,1] neg_hi:[0,1]"
+        : "=&v"(y)
+        : "v"(p), "v"(R), "v"(cp));
+  else
+    asm("v_fma_mixlo_f16 %0, %1, %2, %3 op_sel:[0,0,1] op_sel_hi:[1,0,1]\n\t"
+        "v_fma_mixhi_f16 %0, %1, %2, %3 op_sel:[1,0,1] op_sel_hi:[1,0,1]\n\t"
+        "v_pk_add_f16 %0, %0, %3 op_sel:[0,1] op_sel_hi:[1,1] neg_lo:[0,1] neg_hi:[0,1]"
+        : "=&v"(y)
+        : "v"(p), "v"(R), "v"(cp));
   return y;
+}
+
+// Rounding constants of a pair of 4-blocks (low / high half): with A4 the
+// 4-block maximum, A8 its 8-block maximum and h, q the fp16 floors of 0.875b
+// and 0.4375b, the block's shift is sh = [A8 <= h] + [A4 <= (A8 <= h ? q : h)]
+// = 2 - n with n = [A4 > h] + ([A8 > h] | [A4 > q]), and its constant
+// 1.5 * 2^(10 - sh) has the fp16 bits 0x5E00 + n * 0x400.  Non-negative fp16
+// values order like their bit patterns, so each test is a saturating 16-bit
+// subtraction clamped to 1.
+__device__ __forceinline__ h2_t grid_consts(h2_t a4, h2_t a8, h2_t th_h, h2_t th_q, uint32_t k400, uint32_t k5e00) {
+  h2_t n;
+  uint32_t t, w;
+  asm("v_pk_sub_u16 %0, %3, %5 clamp\n\t"       // n = sat(A4 - h)
+      "v_pk_sub_u16 %1, %4, %5 clamp\n\t"       // t = sat(A8 - h)
+      "v_pk_sub_u16 %2, %3, %6 clamp\n\t"       // w = sat(A4 - q)
+      "v_pk_max_u16 %1, %1, %2\n\t"
+      "v_pk_min_u16 %0, %0, 1 op_sel_hi:[1,0]\n\t"
+      "v_pk_min_u16 %1, %1, 1 op_sel_hi:[1,0]\n\t"
+      "v_pk_add_u16 %0, %0, %1\n\t"
+      "v_pk_mad_u16 %0, %0, %7, %8"
+      : "=&v"(n), "=&v"(t), "=&v"(w)
+      : "v"(a4), "v"(a8), "v"(th_h), "v"(th_q), "v"(k400), "v"(k5e00));
+  return n;
 }
 
 // Global key index (within the 64-key block) held by lane half h at tile t,
@@ -182,6 +243,29 @@ __device__ __forceinline__ h2_t hmax2(h2_t a, h2_t b) {
   asm("v_pk_max_f16 %0, %1, %2" : "=v"(y) : "v"(a), "v"(b));
   return y;
 }
+// Packed maximum of 16 pairs (a tree of 15 v_pk_max_f16 in one block).
+__device__ __forceinline__ h2_t hmax16(const h2_t x[16]) {
+  h2_t y, a1, a2, a3, a4, a5, a6, a7;
+  asm("v_pk_max_f16 %0, %8, %9\n\t"
+      "v_pk_max_f16 %1, %10, %11\n\t"
+      "v_pk_max_f16 %2, %12, %13\n\t"
+      "v_pk_max_f16 %3, %14, %15\n\t"
+      "v_pk_max_f16 %4, %16, %17\n\t"
+      "v_pk_max_f16 %5, %18, %19\n\t"
+      "v_pk_max_f16 %6, %20, %21\n\t"
+      "v_pk_max_f16 %7, %22, %23\n\t"
+      "v_pk_max_f16 %0, %0, %1\n\t"
+      "v_pk_max_f16 %2, %2, %3\n\t"
+      "v_pk_max_f16 %4, %4, %5\n\t"
+      "v_pk_max_f16 %6, %6, %7\n\t"
+      "v_pk_max_f16 %0, %0, %2\n\t"
+      "v_pk_max_f16 %4, %4, %6\n\t"
+      "v_pk_max_f16 %0, %0, %4"
+      : "=&v"(y), "=&v"(a1), "=&v"(a2), "=&v"(a3), "=&v"(a4), "=&v"(a5), "=&v"(a6), "=&v"(a7)
+      : "v"(x[0]), "v"(x[1]), "v"(x[2]), "v"(x[3]), "v"(x[4]), "v"(x[5]), "v"(x[6]), "v"(x[7]), "v"(x[8]),
+        "v"(x[9]), "v"(x[10]), "v"(x[11]), "v"(x[12]), "v"(x[13]), "v"(x[14]), "v"(x[15]));
+  return y;
+}
 // max of the two halves, in both halves
 __device__ __forceinline__ h2_t hmax_halves(h2_t a) {
   h2_t y;
@@ -221,12 +305,12 @@ __device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm,
     for (int g = 0; g < G; ++g) {
       ks[g] = reinterpret_cast<const int*>(cur + lay.k_scale)[(t * G + g) * 32 + col];
       const f16v_t c0 = {};
-      acc[g] = mfma6_rows<0>(ld_op6(cur + lay.k_op + ((size_t)((t * G + g) * 2 + 0) * 64 + lane) * 24), qop[g], c0,
+      acc[g] = mfma6_rows<0>(ld_op6(cur + lay.k_op + (size_t)((t * G + g) * 2 + 0) * kOpRecord, lane), qop[g], c0,
                              ks[g]);
     }
 #pragma unroll
     for (int g = 0; g < G; ++g)
-      acc[g] = mfma6_rows<1>(ld_op6(cur + lay.k_op + ((size_t)((t * G + g) * 2 + 1) * 64 + lane) * 24), qop[g],
+      acc[g] = mfma6_rows<1>(ld_op6(cur + lay.k_op + (size_t)((t * G + g) * 2 + 1) * kOpRecord, lane), qop[g],
                              acc[g], ks[g]);
     float sacc[16];
 #pragma unroll
@@ -247,11 +331,7 @@ __device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm,
         if (64 * J + key_of(t, h, v) > qi) s2[t][v >> 1][v & 1] = ninf;
   }
   // ---- running max (FP16), exchanged with lane l^32.
-  h2_t mx2 = hmax2(s2[0][0], s2[1][0]);
-#pragma unroll
-  for (int t = 0; t < 2; ++t)
-#pragma unroll
-    for (int v2 = 1; v2 < 8; ++v2) mx2 = hmax2(mx2, s2[t][v2]);
+  h2_t mx2 = hmax16(&s2[0][0]);
   mx2 = hmax_halves(max_with_partner(mx2));            // block row max, both halves
   const h2_t mr2 = {st.m_run, st.m_run};
   const h2_t mn2 = hmax2(mr2, mx2);                    // m_new, both halves
@@ -291,13 +371,7 @@ __device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm,
   // x <= 0.875b iff x <= floor16(0.875b) (round-toward-zero conversion).
   const h2_t thr = __builtin_bit_cast(h2_t, __builtin_amdgcn_cvt_pkrtz(0.875f * bval, 0.4375f * bval));
   const h2_t th_h = {thr[0], thr[0]}, th_q = {thr[1], thr[1]};
-  // Per 4-block: sh = [a4 <= h] + [a8 <= h and a4 <= q] = 2 - g4h - max(g8h, g4q)
-  // with g = [x > threshold] in {0,1}; non-negative fp16 values order like
-  // their bit patterns, so the tests are saturating 16-bit subtractions.
-  // The rounding constant C16 = 1.5*2^(10-sh) has bits 0x5E00 + (2-sh)<<10.
-  typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
-  const u16x2 uh = __builtin_bit_cast(u16x2, th_h), uq = __builtin_bit_cast(u16x2, th_q);
-  const u16x2 one2 = {1, 1};
+  const uint32_t k400 = 0x04000400u, k5e00 = 0x5E005E00u;
   h2_t cst[2][2];       // rounding constants of 4-blocks (t, 2jp), (t, 2jp+1)
   h2_t a4s[2][2];
   uint32_t e2bits = 0, e3bits = 0;
@@ -309,12 +383,7 @@ __device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm,
       const h2_t m1 = hmax2(p2[t][4 * jp + 2], p2[t][4 * jp + 3]);   // 4-block 2jp+1
       const h2_t a4 = hmax_pairs(m0, m1);
       const h2_t a8 = max_with_partner(a4);
-      const u16x2 u4 = __builtin_bit_cast(u16x2, a4), u8 = __builtin_bit_cast(u16x2, a8);
-      const u16x2 g4h = __builtin_elementwise_min(__builtin_elementwise_sub_sat(u4, uh), one2);
-      const u16x2 gx = __builtin_elementwise_min(
-          __builtin_elementwise_max(__builtin_elementwise_sub_sat(u8, uh), __builtin_elementwise_sub_sat(u4, uq)), one2);
-      const u16x2 cb = (u16x2){0x5E00, 0x5E00} + ((g4h + gx) << (u16x2){10, 10});
-      cst[t][jp] = __builtin_bit_cast(h2_t, cb);
+      cst[t][jp] = grid_consts(a4, a8, th_h, th_q, k400, k5e00);
       a4s[t][jp] = a4;
       if (DEBUG) {
 #pragma unroll
@@ -337,10 +406,9 @@ __device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm,
   for (int t = 0; t < 2; ++t)
 #pragma unroll
     for (int v2 = 0; v2 < 8; ++v2) {
-      // 4-block j = v2/2 of tile t: constant in half (j & 1) of cst[t][j >> 1]
+      // 4-block j = v2/2 of tile t: its constant is half (j & 1) of cst[t][j >> 1]
       const h2_t cp = cst[t][v2 >> 2];
-      const h2_t c2 = ((v2 >> 1) & 1) ? __builtin_shufflevector(cp, cp, 1, 1) : __builtin_shufflevector(cp, cp, 0, 0);
-      const h2_t tt = fma_grid2(p2[t][v2], R, c2) - c2;
+      const h2_t tt = ((v2 >> 1) & 1) ? grid_round2<1>(p2[t][v2], R, cp) : grid_round2<0>(p2[t][v2], R, cp);
       ov[16 * t + 2 * v2] = tt[0];
       ov[16 * t + 2 * v2 + 1] = tt[1];
     }
@@ -399,11 +467,11 @@ __device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm,
     for (int i = 0; i < 2; ++i) {
       vs[i] = reinterpret_cast<const int*>(cur + lay.v_scale)[32 * (dp + i) + col];
       const f16v_t c0 = {};
-      pv[i] = mfma6_rows<0>(ld_op6(cur + lay.v_op + ((size_t)((dp + i) * 2 + 0) * 64 + lane) * 24), pop, c0, vs[i]);
+      pv[i] = mfma6_rows<0>(ld_op6(cur + lay.v_op + (size_t)((dp + i) * 2 + 0) * kOpRecord, lane), pop, c0, vs[i]);
     }
 #pragma unroll
     for (int i = 0; i < 2; ++i)
-      pv[i] = mfma6_rows<1>(ld_op6(cur + lay.v_op + ((size_t)((dp + i) * 2 + 1) * 64 + lane) * 24), pop, pv[i],
+      pv[i] = mfma6_rows<1>(ld_op6(cur + lay.v_op + (size_t)((dp + i) * 2 + 1) * kOpRecord, lane), pop, pv[i],
                             vs[i]);
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -420,14 +488,12 @@ __device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm,
 }
 
 template <int G, int NORM, bool DEBUG>
-__global__ void __launch_bounds__(256, (G <= 2 ? 2 : 1)) k_attn_hif4(AttnArgs a, int heads_per_wg, int qsub,
+__global__ void __launch_bounds__(256, (G == 1 ? 4 : (G == 2 ? 3 : 1))) k_attn_hif4(AttnArgs a, int heads_per_wg, int qsub,
                                                                       int n_qtiles) {
   constexpr int D = 64 * G;
   constexpr int DT = D / 32;
   constexpr ChunkLayout lay = chunk_layout_hif4(G);
   constexpr int cbytes = (int)lay.bytes;
-  constexpr int n16 = cbytes / 16;
-  constexpr int n_pre = (n16 + 255) / 256;
   extern __shared__ __align__(16) uint8_t smem[];
   const TileMap tm = map_tile(a, heads_per_wg, qsub, n_qtiles);
   if (!tm.wg_live) return;
@@ -517,33 +583,19 @@ __global__ void __launch_bounds__(256, (G <= 2 ? 2 : 1)) k_attn_hif4(AttnArgs a,
   st.inv_rho = 1.0f;
 
   const uint8_t* ws_base = a.ws + ((size_t)(tm.b * a.hkv + tm.hk) * a.NB) * lay.bytes;
-  stage_chunk(smem, ws_base, cbytes);
+  stage_chunk_async<cbytes>(smem, ws_base);
+  wait_async_copies();
   __syncthreads();
 
   for (int J = 0; J < tm.nJ; ++J) {
     const uint8_t* cur = smem + (J & 1) * cbytes;
-    const bool has_next = J + 1 < tm.nJ;
-    u4_t pre[n_pre];
-    {
-      const u4_t* src = reinterpret_cast<const u4_t*>(ws_base + (size_t)(has_next ? J + 1 : J) * cbytes);
-#pragma unroll
-      for (int r = 0; r < n_pre; ++r) {
-        const int i = threadIdx.x + 256 * r;
-        pre[r] = src[i < n16 ? i : n16 - 1];
-      }
-    }
+    // chunk J+1 streams into the other buffer while block J is processed
+    if (J + 1 < tm.nJ) stage_chunk_async<cbytes>(smem + ((J + 1) & 1) * cbytes, ws_base + (size_t)(J + 1) * cbytes);
     if (J < jw_last)
       hif4_block<G, NORM, DEBUG, false>(a, tm, cur, J, lane, h, col, qi, row_ok, qop, bq, ones, st);
     else if (J == jw_last)
       hif4_block<G, NORM, DEBUG, true>(a, tm, cur, J, lane, h, col, qi, row_ok, qop, bq, ones, st);
-    if (has_next) {
-      u4_t* dst = reinterpret_cast<u4_t*>(smem + ((J + 1) & 1) * cbytes);
-#pragma unroll
-      for (int r = 0; r < n_pre; ++r) {
-        const int i = threadIdx.x + 256 * r;
-        if (i < n16) dst[i] = pre[r];
-      }
-    }
+    wait_async_copies();
     __syncthreads();
   }
 

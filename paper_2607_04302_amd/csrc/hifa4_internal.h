@@ -11,6 +11,10 @@ typedef _Float16 half_t;
 
 // Byte layout of one pre-pass chunk = (sequence, kv head, 64-key block).
 // Offsets are multiples of 256 bytes.
+// An FP6 MFMA operand of one wave (64 lanes x 24 bytes) as stored in a chunk:
+// the first 16 bytes of every lane, then the last 8 bytes of every lane.
+constexpr size_t kOpRecord = 64 * 24;
+
 struct ChunkLayout {
   size_t k_op, k_scale, v_op, v_scale, bytes;
 };
@@ -20,15 +24,17 @@ __host__ __device__ constexpr size_t round_up256(size_t x) { return (x + 255) & 
 // HIF4 operands, each group as the two MFMA operands of its split base
 // (operand A = codes, B = zero, codes or negated codes; byte 0 / 1 of the
 // scale word are their E8M0 scales):
-//   K [2 halves][G][2 operands][64 lanes][24 B], K scale words [2][G][32 keys],
-//   V [D/32][2 operands][64 lanes][24 B], V scale words [D].
+//   K [2 halves][G][2 operands] records, K scale words [2][G][32 keys],
+//   V [D/32][2 operands] records, V scale words [D].
 __host__ __device__ constexpr ChunkLayout chunk_layout_hif4(int G) {
   ChunkLayout c{};
   c.k_op = 0;
-  c.k_scale = round_up256((size_t)2 * G * 2 * 64 * 24);
+  c.k_scale = round_up256((size_t)2 * G * 2 * kOpRecord);
   c.v_op = c.k_scale + round_up256((size_t)2 * G * 32 * 4);
-  c.v_scale = c.v_op + round_up256((size_t)(2 * G) * 2 * 64 * 24);
-  c.bytes = c.v_scale + round_up256((size_t)64 * G * 4);
+  c.v_scale = c.v_op + round_up256((size_t)(2 * G) * 2 * kOpRecord);
+  // a multiple of 1 KiB: the attention kernel streams chunks into LDS in
+  // whole-wave pieces of 64 lanes x 16 bytes
+  c.bytes = (c.v_scale + round_up256((size_t)64 * G * 4) + 1023) & ~(size_t)1023;
   return c;
 }
 

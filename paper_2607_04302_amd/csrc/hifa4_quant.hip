@@ -156,12 +156,13 @@ __global__ void __launch_bounds__(256) k_quant_v_canon(const half_t* __restrict_
 // (sequence b, kv head, 64-key block J); wave w < 2G quantizes K half-tile
 // t = w/G, group g = w%G; wave w >= 2G quantizes V channel tile w-2G.
 // Writes, for the chunk:
-//   K operands [2 halves][G groups][2][64 lanes][6 dwords]: lane l holds key
+//   K operands [2 halves][G groups][2] operand records (64 lanes x dwords
+//     0..3, then 64 lanes x dwords 4..5 of the lane's 6): lane l holds key
 //     32t + l%32 and channels 64g + 32(l/32) + [0,32) in FP6 E2M3, i.e. the
 //     A operand of S^T = K^ Q^T for the 32x32x64 MFMA, as the two operands of
 //     the key's split base (below);
 //   K scale words [2][G][32]: their two E8M0 bytes per key and group;
-//   V operands [D/32 tiles][2][64 lanes][6 dwords]: lane l holds channel
+//   V operands [D/32 tiles][2] operand records: lane l holds channel
 //     32dt + l%32 and, at FP6 slot s, the key 32(s/16) + 8((s%16)/4) +
 //     4(l/32) + s%4 -- the key order in which the attention kernel's P^
 //     operand arrives (the S^T accumulator registers of both 32-key halves in
@@ -184,17 +185,23 @@ __device__ __forceinline__ uint32_t split_scale_word(uint32_t base) {
   return sa | (sb << 8);
 }
 
-// Stores operand A (the lane's 24 code bytes) at dst and operand B 64 lanes
-// (1536 bytes) later.  The E2M3 sign is bit 5 of each 6-bit field.
-__device__ __forceinline__ void store_split_operand(int* dst, const i6_t& pk, uint32_t base) {
+// Stores a lane's operand A (its 24 code bytes) into the operand record at
+// rec and operand B into the next record.  A record holds dwords 0..3 of the
+// 64 lanes (16 bytes each), then dwords 4..5 (8 bytes each).  The E2M3 sign is
+// bit 5 of each 6-bit field.
+__device__ __forceinline__ void store_split_operand(uint8_t* rec, int lane, const i6_t& pk, uint32_t base) {
   constexpr uint32_t kSign[3] = {0x20820820u, 0x08208208u, 0x82082082u};   // fields 6s+5, period 96 bits
   const uint32_t m = base & 3u;
+  uint32_t wa[6], wb[6];
 #pragma unroll
   for (int i = 0; i < 6; ++i) {
-    const uint32_t w = (uint32_t)pk[i];
-    dst[i] = (int)w;
-    dst[64 * 6 + i] = (int)(m == 0u ? 0u : (m == 3u ? w ^ kSign[i % 3] : w));
+    wa[i] = (uint32_t)pk[i];
+    wb[i] = m == 0u ? 0u : (m == 3u ? wa[i] ^ kSign[i % 3] : wa[i]);
   }
+  *reinterpret_cast<uint4*>(rec + 16 * lane) = make_uint4(wa[0], wa[1], wa[2], wa[3]);
+  *reinterpret_cast<uint2*>(rec + 1024 + 8 * lane) = make_uint2(wa[4], wa[5]);
+  *reinterpret_cast<uint4*>(rec + kOpRecord + 16 * lane) = make_uint4(wb[0], wb[1], wb[2], wb[3]);
+  *reinterpret_cast<uint2*>(rec + kOpRecord + 1024 + 8 * lane) = make_uint2(wb[4], wb[5]);
 }
 
 __global__ void __launch_bounds__(1024) k_prep_kv_hif4(const half_t* __restrict__ k, const half_t* __restrict__ v,
@@ -238,8 +245,7 @@ __global__ void __launch_bounds__(1024) k_prep_kv_hif4(const half_t* __restrict_
 #pragma unroll
     for (int c = 0; c < 32; ++c) hv[c] = (half_t)o[c];
     const i6_t pk = __builtin_amdgcn_cvt_scalef32_pk32_fp6_f16(hv, 1.0f);
-    int* dst = reinterpret_cast<int*>(chunk + lay.k_op + ((size_t)(t * G + g) * 2 * 64 + lane) * 24);
-    store_split_operand(dst, pk, gm.base);
+    store_split_operand(chunk + lay.k_op + (size_t)(t * G + g) * 2 * kOpRecord, lane, pk, gm.base);
     if (h == 0)
       reinterpret_cast<uint32_t*>(chunk + lay.k_scale)[(t * G + g) * 32 + (lane & 31)] = split_scale_word(gm.base);
   } else if (wave < 4 * G) {
@@ -258,8 +264,7 @@ __global__ void __launch_bounds__(1024) k_prep_kv_hif4(const half_t* __restrict_
 #pragma unroll
     for (int c = 0; c < 32; ++c) hv[c] = (half_t)o[c];
     const i6_t pk = __builtin_amdgcn_cvt_scalef32_pk32_fp6_f16(hv, 1.0f);
-    int* dst = reinterpret_cast<int*>(chunk + lay.v_op + ((size_t)dt * 2 * 64 + lane) * 24);
-    store_split_operand(dst, pk, gm.base);
+    store_split_operand(chunk + lay.v_op + (size_t)dt * 2 * kOpRecord, lane, pk, gm.base);
     if (h == 0) reinterpret_cast<uint32_t*>(chunk + lay.v_scale)[d] = split_scale_word(gm.base);
   }
 }
