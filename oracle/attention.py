@@ -14,8 +14,9 @@ Readings fixed here (the paper is silent on them):
     contraction axis of its GEMM;
   * scores: per 64-channel group g the dot t_g of the dequantized operands is
     exact; S_acc = (((t_0 + t_1) + t_2) + ...) with fp32 round-to-nearest
-    additions; S2 = fp16(S_acc * c), the exact product rounded once to fp16,
-    with c = fp32(log2(e)/sqrt(D)), so the softmax runs in base 2
+    additions; S2 = fp16(fp32(S_acc * c)): the product is rounded to fp32,
+    then to fp16 (both to nearest even), with c = fp32(log2(e)/sqrt(D)), so
+    the softmax runs in base 2
     (2^(S2-m) equals exp(S/sqrt(D) - m') exactly in real arithmetic);
   * running max m and the weights are fp16: m_new = max(m, rowmax S2),
     x = fp16(S2 - m_new), P16 = E(x), r = E(fp16(m - m_new));
@@ -71,26 +72,27 @@ def quantize_tokens(v):
 
 
 def scores_hif4(qhat, khat, head_dim):
-    """S2 = fp16(S_acc * c) from dequantized operands (float64 [n, D] and
-    [L, D]).  Each group dot is exact in float64 (integer grid, at most 22
+    """S2 = fp16(fp32(S_acc * c)) from dequantized operands (float64 [n, D]
+    and [L, D]).  Each group dot is exact in float64 (integer grid, at most 22
     significant bits) and in fp32; the fp32 partial sums round to nearest; the
-    product S_acc * c of two fp32 values is exact in float64 and is rounded
-    once to fp16."""
+    scaled score S_acc * c is rounded to fp32 and then to fp16 (both round to
+    nearest even): the scores are scaled in the fp32 accumulator precision and
+    handed to the FP16 softmax."""
     c = score_scale(head_dim)
     s_acc = None
     for g in range(head_dim // 64):
         sl = slice(64 * g, 64 * g + 64)
         t = (qhat[:, sl] @ khat[:, sl].T).astype(np.float32)   # exact
         s_acc = t if s_acc is None else (s_acc + t)             # fp32 RN add
-    return (s_acc.astype(np.float64) * np.float64(c)).astype(np.float16)
+    return (s_acc * c).astype(np.float32).astype(np.float16)
 
 
 def scores_fp16(q, k, head_dim):
-    """FP16-operand variant: fp32 dot of the fp16 operands; times c, rounded
-    once to fp16."""
+    """FP16-operand variant: fp32 dot of the fp16 operands; times c in fp32,
+    then to fp16."""
     c = score_scale(head_dim)
     s = (q.astype(np.float64) @ k.astype(np.float64).T).astype(np.float32)
-    return (s.astype(np.float64) * np.float64(c)).astype(np.float16)
+    return (s * c).astype(np.float32).astype(np.float16)
 
 
 def online_softmax(s2, vop, rows, length, quantize_p, want_p=False, arith="contract"):

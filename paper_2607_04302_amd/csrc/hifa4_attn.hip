@@ -272,13 +272,22 @@ __device__ __forceinline__ h2_t hmax_halves(h2_t a) {
   asm("v_pk_max_f16 %0, %1, %1 op_sel:[0,1] op_sel_hi:[1,0]" : "=v"(y) : "v"(a));
   return y;
 }
-// (a.lo, b.lo) and (a.hi, b.hi) maxima of two packed pairs: max(a.lo, a.hi),
-// max(b.lo, b.hi) in the low and high halves.
+// max(a.lo, a.hi) in the low half and max(b.lo, b.hi) in the high half
+// (two SDWA maxima in one block).
 __device__ __forceinline__ h2_t hmax_pairs(h2_t a, h2_t b) {
   h2_t y;
-  asm("v_pk_max_f16 %0, %1, %2 op_sel:[0,0] op_sel_hi:[1,1]" : "=v"(y) : "v"(__builtin_shufflevector(a, b, 0, 2)),
-      "v"(__builtin_shufflevector(a, b, 1, 3)));
+  asm("v_max_f16_sdwa %0, %1, %1 dst_sel:WORD_0 dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:WORD_1\n\t"
+      "v_max_f16_sdwa %0, %2, %2 dst_sel:WORD_1 dst_unused:UNUSED_PRESERVE src0_sel:WORD_0 src1_sel:WORD_1"
+      : "=&v"(y)
+      : "v"(a), "v"(b));
   return y;
+}
+
+// The value of lane l^32 through the LDS crossbar (ds_bpermute; `addr` is
+// 4 * (l ^ 32)).  Used where several exchanges are independent so that their
+// latency overlaps and the VALU stays free.
+__device__ __forceinline__ uint32_t partner_bperm(uint32_t v, int addr) {
+  return (uint32_t)__builtin_amdgcn_ds_bpermute(addr, (int)v);
 }
 
 template <int G>
@@ -295,7 +304,7 @@ __device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm,
                                            const float (&bq)[G], const i8_t& ones, Hif4State<G>& st) {
   constexpr int DT = 2 * G;
   constexpr ChunkLayout lay = chunk_layout_hif4(G);
-  // ---- scores: S2 = fp16((sum_g acc_g * b_q/4) * c).
+  // ---- scores: S2 = fp16(fp32((sum_g acc_g * b_q/4) * c)).
   h2_t s2[2][8];
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
@@ -320,7 +329,7 @@ __device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm,
       for (int g = 1; g < G; ++g) sacc[v] = __builtin_fmaf(acc[g][v], bq[g], sacc[v]);
     }
 #pragma unroll
-    for (int v2 = 0; v2 < 8; ++v2) s2[t][v2] = mul2_rn16(sacc[2 * v2], sacc[2 * v2 + 1], a.c);
+    for (int v2 = 0; v2 < 8; ++v2) s2[t][v2] = scale2_to_f16(sacc[2 * v2], sacc[2 * v2 + 1], a.c);
   }
   if (MASK) {
     const half_t ninf = (half_t)(-__builtin_inff());
@@ -373,18 +382,25 @@ __device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm,
   const h2_t th_h = {thr[0], thr[0]}, th_q = {thr[1], thr[1]};
   const uint32_t k400 = 0x04000400u, k5e00 = 0x5E005E00u;
   h2_t cst[2][2];       // rounding constants of 4-blocks (t, 2jp), (t, 2jp+1)
-  h2_t a4s[2][2];
+  h2_t a4s[2][2], a4p[2][2];
   uint32_t e2bits = 0, e3bits = 0;
+  const int paddr = 4 * (lane ^ 32);
 #pragma unroll
   for (int t = 0; t < 2; ++t)
 #pragma unroll
     for (int jp = 0; jp < 2; ++jp) {
       const h2_t m0 = hmax2(p2[t][4 * jp], p2[t][4 * jp + 1]);       // 4-block 2jp, two partial maxima
       const h2_t m1 = hmax2(p2[t][4 * jp + 2], p2[t][4 * jp + 3]);   // 4-block 2jp+1
-      const h2_t a4 = hmax_pairs(m0, m1);
-      const h2_t a8 = max_with_partner(a4);
+      a4s[t][jp] = hmax_pairs(m0, m1);
+      a4p[t][jp] = __builtin_bit_cast(h2_t, partner_bperm(__builtin_bit_cast(uint32_t, a4s[t][jp]), paddr));
+    }
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int jp = 0; jp < 2; ++jp) {
+      const h2_t a4 = a4s[t][jp];
+      const h2_t a8 = hmax2(a4, a4p[t][jp]);
       cst[t][jp] = grid_consts(a4, a8, th_h, th_q, k400, k5e00);
-      a4s[t][jp] = a4;
       if (DEBUG) {
 #pragma unroll
         for (int e = 0; e < 2; ++e) {
@@ -393,7 +409,7 @@ __device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm,
           const bool e3 = a4[e] <= (e2 ? th_q[e] : th_h[e]);
           e2bits |= (uint32_t)e2 << (4 * t + j);
           e3bits |= (uint32_t)e3 << (8 * t + 2 * j + h);
-          const bool e3o = partner_h2(a4, h)[e] <= (e2 ? th_q[e] : th_h[e]);
+          const bool e3o = a4p[t][jp][e] <= (e2 ? th_q[e] : th_h[e]);
           e3bits |= (uint32_t)e3o << (8 * t + 2 * j + (h ^ 1));
         }
       }
@@ -672,8 +688,7 @@ __global__ void __launch_bounds__(256) k_attn_fp16(AttnArgs a, int heads_per_wg,
         }
 #pragma unroll
         for (int v2 = 0; v2 < 8; ++v2) {
-          s2[t][v2][0] = (half_t)(acc[2 * v2] * a.c);
-          s2[t][v2][1] = (half_t)(acc[2 * v2 + 1] * a.c);
+          s2[t][v2] = scale2_to_f16(acc[2 * v2], acc[2 * v2 + 1], a.c);
         }
       }
       if (64 * J + 63 > tm.qw) {

@@ -112,6 +112,15 @@ __device__ __forceinline__ half_t mul_rn16(float a, float b) {
   return y;
 }
 
+// Pack fp16(fp32(a*c)) and fp16(fp32(b*c)): the products are rounded to fp32,
+// then converted to fp16 (round to nearest even) by one packed conversion.
+__device__ __forceinline__ h2_t scale2_to_f16(float a, float b, float c) {
+  const float ya = a * c, yb = b * c;
+  h2_t y;
+  asm("v_cvt_pk_f16_f32 %0, %1, %2" : "=v"(y) : "v"(ya), "v"(yb));
+  return y;
+}
+
 // Pack fp16(a*c) and fp16(b*c) (each rounded once) into one register.
 __device__ __forceinline__ h2_t mul2_rn16(float a, float b, float c) {
   h2_t y;

@@ -180,3 +180,23 @@ def test_smoothing_preserves_qk_direction():
         a = qt[:, h].astype(np.float64) @ kt[:, 0].astype(np.float64).T
         b = q[:, h].astype(np.float64) @ k[:, 0].astype(np.float64).T
         assert np.max(np.abs(a - b)) < 2e-2 * np.abs(b).max()
+
+
+def test_score_rounding_goes_through_fp32():
+    """S2 = fp16(fp32(S_acc * c)): the scaled score is rounded to fp32 first.
+    Witness: S_acc = 1.386971354484558 (an fp32 value), D = 64.  The exact
+    product S_acc * c lies above the fp16 midpoint M = 0.2501220703125 of
+    0.25 and 0.250244140625 but rounds to M in fp32; rounding M to nearest
+    even gives 0.25, while a single rounding of the exact product would give
+    0.250244140625."""
+    from fractions import Fraction
+    s_acc = np.float32(1.386971354484558)
+    c = attention.score_scale(64)
+    mid = Fraction(0.25) + Fraction(1, 2 ** 13)
+    assert Fraction(float(s_acc)) * Fraction(float(c)) > mid          # single rounding -> upper
+    qhat = np.zeros((1, 64))
+    khat = np.zeros((1, 64))
+    qhat[0, 0] = float(s_acc)
+    khat[0, 0] = 1.0
+    s2 = attention.scores_hif4(qhat, khat, 64)
+    assert s2.dtype == np.float16 and float(s2[0, 0]) == 0.25
