@@ -220,6 +220,22 @@ __device__ __forceinline__ int key_of(int t, int h, int v) { return 32 * t + 8 *
 // differs.  A factor r = 0 (a running max that grows by more than 24 in log2
 // units after the first block) wipes the history, exactly as r*O does.
 
+// Wave issue priority from the work left.  A SIMD issues from the oldest
+// ready wave first, so without this the youngest of the co-resident
+// workgroups (the one dispatched last) is starved and finishes last even
+// when it has the least work.  Raising the priority of the workgroups with
+// the most blocks left makes the co-resident workgroups of a CU finish
+// together (longest remaining work first).
+__device__ __forceinline__ void set_priority_by_work_left(int blocks_left) {
+  const int p = blocks_left >= 48 ? 3 : (blocks_left >= 24 ? 2 : (blocks_left >= 8 ? 1 : 0));
+  switch (p) {
+    case 3: __builtin_amdgcn_s_setprio(3); break;
+    case 2: __builtin_amdgcn_s_setprio(2); break;
+    case 1: __builtin_amdgcn_s_setprio(1); break;
+    default: __builtin_amdgcn_s_setprio(0); break;
+  }
+}
+
 // fp16 exponential of four packed pairs; the four low-half results are
 // written before the first SDWA high-half instruction reads its destination,
 // which keeps the transcendental result latency out of the way without nops.
@@ -604,6 +620,7 @@ __global__ void __launch_bounds__(256, (G == 1 ? 4 : (G == 2 ? 3 : 1))) k_attn_h
   __syncthreads();
 
   for (int J = 0; J < tm.nJ; ++J) {
+    set_priority_by_work_left(tm.nJ - J);
     const uint8_t* cur = smem + (J & 1) * cbytes;
     // chunk J+1 streams into the other buffer while block J is processed
     if (J + 1 < tm.nJ) stage_chunk_async<cbytes>(smem + ((J + 1) & 1) * cbytes, ws_base + (size_t)(J + 1) * cbytes);
@@ -674,6 +691,7 @@ __global__ void __launch_bounds__(256) k_attn_fp16(AttnArgs a, int heads_per_wg,
   __syncthreads();
 
   for (int J = 0; J < tm.nJ; ++J) {
+    set_priority_by_work_left(tm.nJ - J);
     const uint8_t* cur = smem + (J & 1) * cbytes;
     const bool has_next = J + 1 < tm.nJ;
     if (tm.active && J <= jw_last) {
