@@ -70,22 +70,39 @@ __device__ __forceinline__ void stage_chunk(uint8_t* lds, const uint8_t* __restr
   for (int i = threadIdx.x; i < bytes / 16; i += blockDim.x) dst[i] = src[i];
 }
 
-// Start an asynchronous copy of one chunk (BYTES, a multiple of 16) from
-// global memory straight into LDS (global_load_lds, 16 bytes per lane; lane i
-// of a wave lands at the wave's LDS base + 16 i).  Completion is tracked by
-// vmcnt: the caller waits with vmcnt(0) and a barrier before reading.
+// Asynchronous copy of one chunk (BYTES, a multiple of 1 KiB) from global
+// memory straight into LDS (global_load_lds, 16 bytes per lane; lane i of a
+// wave lands at the wave's LDS base + 16 i), in pieces of 256 lanes x 16
+// bytes.  Completion is tracked by vmcnt: the caller waits with vmcnt(0) and
+// a barrier before reading.  Issuing a piece stalls the wave while the
+// texture path is busy, so the block code spreads the pieces over its phases
+// instead of issuing the whole chunk at once.
+struct ChunkStream {
+  uint8_t* dst;            // LDS buffer
+  const uint8_t* src;      // global chunk, or nullptr: nothing to stream
+};
+
+template <int BYTES>
+__device__ __forceinline__ void stream_piece(const ChunkStream& cs, int r) {
+  constexpr int n16 = BYTES / 16;
+  if (!cs.src || r * 256 >= n16) return;
+  const int wave = threadIdx.x >> 6;
+  const int i = threadIdx.x + 256 * r;
+  if (256 * r + 64 * wave < n16)          // whole waves: n16 is a multiple of 64
+    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(cs.src + 16 * (size_t)i),
+                                     (__attribute__((address_space(3))) void*)(cs.dst + 4096 * r + 1024 * wave), 16, 0,
+                                     0);
+}
+
+template <int BYTES>
+__device__ __forceinline__ void stream_pieces_from(const ChunkStream& cs, int r0) {
+#pragma unroll
+  for (int r = r0; r < (BYTES / 16 + 255) / 256; ++r) stream_piece<BYTES>(cs, r);
+}
+
 template <int BYTES>
 __device__ __forceinline__ void stage_chunk_async(uint8_t* lds, const uint8_t* __restrict__ g) {
-  constexpr int n16 = BYTES / 16;
-  const int wave = threadIdx.x >> 6;
-#pragma unroll
-  for (int r = 0; r < (n16 + 255) / 256; ++r) {
-    const int i = threadIdx.x + 256 * r;
-    if (256 * r + 64 * wave < n16)          // whole waves: n16 is a multiple of 64
-      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(g + 16 * (size_t)i),
-                                       (__attribute__((address_space(3))) void*)(lds + 4096 * r + 1024 * wave), 16,
-                                       0, 0);
-  }
+  stream_pieces_from<BYTES>(ChunkStream{lds, g}, 0);
 }
 
 __device__ __forceinline__ void wait_async_copies() { __builtin_amdgcn_s_waitcnt(0x0F70); }   // vmcnt(0)
@@ -317,13 +334,16 @@ struct Hif4State {
 template <int G, int NORM, bool DEBUG, bool MASK>
 __device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm, const uint8_t* cur, int J, int lane,
                                            int h, int col, int qi, bool row_ok, const i8_t (&qop)[G],
-                                           const float (&bq)[G], const i8_t& ones, Hif4State<G>& st) {
+                                           const float (&bq)[G], const i8_t& ones, Hif4State<G>& st,
+                                           const ChunkStream& cs) {
   constexpr int DT = 2 * G;
   constexpr ChunkLayout lay = chunk_layout_hif4(G);
+  constexpr int CB = (int)lay.bytes;
   // ---- scores: S2 = fp16(fp32((sum_g acc_g * b_q/4) * c)).
   h2_t s2[2][8];
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
+    stream_piece<CB>(cs, t);
     f16v_t acc[G];
     int ks[G];
 #pragma unroll
@@ -337,6 +357,7 @@ __device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm,
     for (int g = 0; g < G; ++g)
       acc[g] = mfma6_rows<1>(ld_op6(cur + lay.k_op + (size_t)((t * G + g) * 2 + 1) * kOpRecord, lane), qop[g],
                              acc[g], ks[g]);
+    stream_piece<CB>(cs, 2 + t);
     float sacc[16];
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
@@ -360,6 +381,7 @@ __device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm,
   mx2 = hmax_halves(max_with_partner(mx2));            // block row max, both halves
   const h2_t mr2 = {st.m_run, st.m_run};
   const h2_t mn2 = hmax2(mr2, mx2);                    // m_new, both halves
+  stream_piece<CB>(cs, 4);
   // ---- P = 2^(S2 - m_new); r = 2^(m - m_new) and the block max A = 2^(mx - m_new).
   h2_t p2[2][8];
 #pragma unroll
@@ -385,6 +407,7 @@ __device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm,
     psum = add_with_partner(psum);
   }
 
+  stream_piece<CB>(cs, 5);
   // ---- P^ = HIF4(P) over the block's 64 keys (P-Reordering).
   // The lane's 4-block (t, j) holds keys 32t + 8j + 4h + [0,4), i.e. the
   // packed registers p2[t][2j] and p2[t][2j+1].  Maxima are packed in pairs
@@ -469,6 +492,7 @@ __device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm,
       a.dbg_meta[((size_t)tm.hq * a.total_tokens + tm.t0 + qi) * a.NB + J] = base | (e2bits << 8) | (e3bits << 16);
   }
 
+  stream_piece<CB>(cs, 6);
   // ---- deferred rescale bookkeeping (lane-uniform factors).
   if (__builtin_expect(J > 0 && __builtin_amdgcn_ballot_w64(r == 0.0f) != 0, 0)) {
     // history wiped for some rows: O <- 0*O, l <- 0*l there
@@ -510,6 +534,7 @@ __device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm,
 #pragma unroll
       for (int v = 0; v < 16; ++v) st.O[dp + i][v] = __builtin_fmaf(pv[i][v], wp, st.O[dp + i][v]);
   }
+  stream_pieces_from<CB>(cs, 7);
   if (NORM == 1) {
     st.l_star = __builtin_fmaf(psum, st.inv_rho, st.l_star);
   } else {
@@ -623,11 +648,13 @@ __global__ void __launch_bounds__(256, (G == 1 ? 4 : (G == 2 ? 3 : 1))) k_attn_h
     set_priority_by_work_left(tm.nJ - J);
     const uint8_t* cur = smem + (J & 1) * cbytes;
     // chunk J+1 streams into the other buffer while block J is processed
-    if (J + 1 < tm.nJ) stage_chunk_async<cbytes>(smem + ((J + 1) & 1) * cbytes, ws_base + (size_t)(J + 1) * cbytes);
+    const ChunkStream cs{smem + ((J + 1) & 1) * cbytes, J + 1 < tm.nJ ? ws_base + (size_t)(J + 1) * cbytes : nullptr};
     if (J < jw_last)
-      hif4_block<G, NORM, DEBUG, false>(a, tm, cur, J, lane, h, col, qi, row_ok, qop, bq, ones, st);
+      hif4_block<G, NORM, DEBUG, false>(a, tm, cur, J, lane, h, col, qi, row_ok, qop, bq, ones, st, cs);
     else if (J == jw_last)
-      hif4_block<G, NORM, DEBUG, true>(a, tm, cur, J, lane, h, col, qi, row_ok, qop, bq, ones, st);
+      hif4_block<G, NORM, DEBUG, true>(a, tm, cur, J, lane, h, col, qi, row_ok, qop, bq, ones, st, cs);
+    else
+      stream_pieces_from<cbytes>(cs, 0);
     wait_async_copies();
     __syncthreads();
   }
