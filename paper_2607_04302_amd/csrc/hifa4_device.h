@@ -150,6 +150,20 @@ __device__ __forceinline__ half_t div_rn16(float k, float s) {
   return (above == nb_above) ? nb : h;
 }
 
+// The same quotient from a reciprocal rs = RN32(1/s): k*rs = (k/s)(1 + d)
+// with |d| <= 2^-24, so q = RN32(k*rs) lies within 1.5 fp32 ulps of k/s and
+// RN16(q) = RN16(k/s) unless q's bits below the fp16 precision (the low 13
+// mantissa bits) are within 3 of the halfway pattern 0x1000, or q is in
+// fp16's subnormal range; those take div_rn16.
+__device__ __forceinline__ half_t div_rn16_rcp(float k, float s, float rs) {
+  const float q = k * rs;
+  const uint32_t b = __float_as_uint(q);
+  const bool near_mid = ((b & 0x1FFFu) - 0xFFDu) < 7u;
+  const bool tiny = (b & 0x7F800000u) < 0x38800000u && (b & 0x7FFFFFFFu) != 0u;
+  if (__builtin_expect(near_mid || tiny, 0)) return div_rn16(k, s);
+  return (half_t)q;
+}
+
 __device__ __forceinline__ float shfl_xor32(float v) {
   return __shfl_xor(v, 32);
 }

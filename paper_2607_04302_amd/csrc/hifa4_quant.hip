@@ -20,9 +20,13 @@ __device__ __forceinline__ int seq_len(const int* cu, int b, int S) {
 // Load 32 consecutive fp16 channels of one (token, head) row and apply the
 // Smooth-QK scale: q~ = fp16(q*s) and k~ = fp16(k/s), the exact product or
 // quotient rounded once.  Returns the values as fp32.
+// For K, `rs` may hold the reciprocals RN32(1/s) of the same 32 channels;
+// the quotient then comes from div_rn16_rcp (same result, mostly without a
+// division).
 template <bool kIsK>
 __device__ __forceinline__ void load_smoothed32(const half_t* __restrict__ src,
-                                                const float* __restrict__ s, float x[32]) {
+                                                const float* __restrict__ s, float x[32],
+                                                const float* rs = nullptr) {
   const uint4* p = reinterpret_cast<const uint4*>(src);
 #pragma unroll
   for (int v = 0; v < 4; ++v) {
@@ -32,8 +36,13 @@ __device__ __forceinline__ void load_smoothed32(const half_t* __restrict__ src,
     for (int i = 0; i < 8; ++i) x[8 * v + i] = (float)h[i];
   }
   if (s) {
+    if (kIsK && rs) {
 #pragma unroll
-    for (int c = 0; c < 32; ++c) x[c] = (float)(kIsK ? div_rn16(x[c], s[c]) : mul_rn16(x[c], s[c]));
+      for (int c = 0; c < 32; ++c) x[c] = (float)div_rn16_rcp(x[c], s[c], rs[c]);
+    } else {
+#pragma unroll
+      for (int c = 0; c < 32; ++c) x[c] = (float)(kIsK ? div_rn16(x[c], s[c]) : mul_rn16(x[c], s[c]));
+    }
   }
 }
 
@@ -152,9 +161,10 @@ __global__ void __launch_bounds__(256) k_quant_v_canon(const half_t* __restrict_
 }
 
 // ---------------------------------------------------------------------------
-// Attention pre-pass (HIF4 operands).  One workgroup of 4G waves per
-// (sequence b, kv head, 64-key block J); wave w < 2G quantizes K half-tile
-// t = w/G, group g = w%G; wave w >= 2G quantizes V channel tile w-2G.
+// Attention pre-pass (HIF4 operands).  Two workgroups of 2G waves per
+// (sequence b, kv head, 64-key block J): in the K workgroup wave w quantizes
+// K half-tile t = w/G, group g = w%G; in the V workgroup wave w quantizes V
+// channel tile w.
 // Writes, for the chunk:
 //   K operands [2 halves][G groups][2] operand records (64 lanes x dwords
 //     0..3, then 64 lanes x dwords 4..5 of the lane's 6): lane l holds key
@@ -204,38 +214,40 @@ __device__ __forceinline__ void store_split_operand(uint8_t* rec, int lane, cons
   *reinterpret_cast<uint2*>(rec + kOpRecord + 1024 + 8 * lane) = make_uint2(wb[4], wb[5]);
 }
 
-__global__ void __launch_bounds__(1024) k_prep_kv_hif4(const half_t* __restrict__ k, const half_t* __restrict__ v,
-                                                       const float* __restrict__ s, const int* __restrict__ cu,
-                                                       uint8_t* __restrict__ ws, int S, int NB, int heads_kv,
-                                                       int G) {
-  extern __shared__ __align__(16) half_t vt[];       // [64 keys][D] tile of V
-  const int J = blockIdx.x, hk = blockIdx.y, b = blockIdx.z;
+__global__ void __launch_bounds__(512) k_prep_kv_hif4(const half_t* __restrict__ k, const half_t* __restrict__ v,
+                                                      const float* __restrict__ s, const int* __restrict__ cu,
+                                                      uint8_t* __restrict__ ws, int S, int NB, int heads_kv, int G) {
+  // workgroup (J, hk, 2b + role): role 0 quantizes K, role 1 V, of block J
+  extern __shared__ __align__(16) uint8_t sm[];
+  const int J = blockIdx.x, hk = blockIdx.y, b = blockIdx.z >> 1;
+  const bool is_v = (blockIdx.z & 1) != 0;
   const int D = 64 * G;
   const int t0 = seq_start(cu, b, S);
   const int L = seq_len(cu, b, S);
   if (64 * J >= L) return;
   const ChunkLayout lay = chunk_layout_hif4(G);
   uint8_t* chunk = ws + ((size_t)(b * heads_kv + hk) * NB + J) * lay.bytes;
-  // stage V rows [64J, 64J+64) of this head, zero past the sequence end
-  const int n16 = 64 * D / 8;
-  for (int i = threadIdx.x; i < n16; i += blockDim.x) {
-    const int key = i / (D / 8), c8 = i % (D / 8);
-    const int pos = 64 * J + key;
-    uint4 val = make_uint4(0, 0, 0, 0);
-    if (pos < L) val = *reinterpret_cast<const uint4*>(v + ((size_t)(t0 + pos) * heads_kv + hk) * D + 8 * c8);
-    reinterpret_cast<uint4*>(vt)[i] = val;
-  }
-  __syncthreads();
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, h = lane >> 5;
   float x[32], o[32];
-  if (wave < 2 * G) {
+  if (!is_v) {
+    // this head's smoothing scales and their reciprocals (one division per
+    // channel), staged in LDS
+    float* rs = reinterpret_cast<float*>(sm);
+    float* ss = rs + D;
+    if (s) {
+      for (int c = threadIdx.x; c < D; c += blockDim.x) {
+        const float sc = s[(size_t)hk * D + c];
+        ss[c] = sc;
+        rs[c] = 1.0f / sc;
+      }
+      __syncthreads();
+    }
     const int t = wave / G, g = wave % G;
     const int key = 32 * t + (lane & 31);
     const int pos = 64 * J + key;
     if (pos < L) {
       const half_t* src = k + ((size_t)(t0 + pos) * heads_kv + hk) * D + 64 * g + 32 * h;
-      const float* sp = s ? s + (size_t)hk * D + 64 * g + 32 * h : nullptr;
-      load_smoothed32<true>(src, sp, x);
+      load_smoothed32<true>(src, s ? ss + 64 * g + 32 * h : nullptr, x, rs + 64 * g + 32 * h);
     } else {
 #pragma unroll
       for (int c = 0; c < 32; ++c) x[c] = 0.0f;
@@ -248,8 +260,19 @@ __global__ void __launch_bounds__(1024) k_prep_kv_hif4(const half_t* __restrict_
     store_split_operand(chunk + lay.k_op + (size_t)(t * G + g) * 2 * kOpRecord, lane, pk, gm.base);
     if (h == 0)
       reinterpret_cast<uint32_t*>(chunk + lay.k_scale)[(t * G + g) * 32 + (lane & 31)] = split_scale_word(gm.base);
-  } else if (wave < 4 * G) {
-    const int dt = wave - 2 * G;
+  } else {
+    // stage V rows [64J, 64J+64) of this head, zero past the sequence end
+    half_t* vt = reinterpret_cast<half_t*>(sm);        // [64 keys][D]
+    const int n16 = 64 * D / 8;
+    for (int i = threadIdx.x; i < n16; i += blockDim.x) {
+      const int key = i / (D / 8), c8 = i % (D / 8);
+      const int pos = 64 * J + key;
+      uint4 val = make_uint4(0, 0, 0, 0);
+      if (pos < L) val = *reinterpret_cast<const uint4*>(v + ((size_t)(t0 + pos) * heads_kv + hk) * D + 8 * c8);
+      reinterpret_cast<uint4*>(vt)[i] = val;
+    }
+    __syncthreads();
+    const int dt = wave;
     const int d = 32 * dt + (lane & 31);
     // slot s = 4kk + i holds key 32t + 8j + 4h + i of the lane's 4-block
     // kk = (t, j), which is the quantizer's block order as well
@@ -408,8 +431,8 @@ hipError_t launch_prep_kv(const half_t* k, const half_t* v, const float* s, cons
   if (fp16)
     k_prep_kv_fp16<<<grid, dim3(256), 0, st>>>(k, v, cu, ws, S, NB, heads_kv, D);
   else
-    k_prep_kv_hif4<<<grid, dim3(64 * 4 * (D / 64)), 64 * D * sizeof(half_t), st>>>(k, v, s, cu, ws, S, NB, heads_kv,
-                                                                                   D / 64);
+    k_prep_kv_hif4<<<dim3(NB, heads_kv, 2 * batch), dim3(64 * 2 * (D / 64)), 64 * D * sizeof(half_t), st>>>(
+        k, v, s, cu, ws, S, NB, heads_kv, D / 64);
   return hipGetLastError();
 }
 
