@@ -73,25 +73,27 @@ __device__ __forceinline__ void stage_chunk(uint8_t* lds, const uint8_t* __restr
 // Asynchronous copy of one chunk (BYTES, a multiple of 1 KiB) from global
 // memory straight into LDS (global_load_lds, 16 bytes per lane; lane i of a
 // wave lands at the wave's LDS base + 16 i), in pieces of 256 lanes x 16
-// bytes.  Completion is tracked by vmcnt: the caller waits with vmcnt(0) and
+// bytes.  On the last block of a tile the current chunk is streamed into the
+// idle buffer again, which keeps the block code free of branches.  Completion is tracked by vmcnt: the caller waits with vmcnt(0) and
 // a barrier before reading.  Issuing a piece stalls the wave while the
 // texture path is busy, so the block code spreads the pieces over its phases
 // instead of issuing the whole chunk at once.
 struct ChunkStream {
   uint8_t* dst;            // LDS buffer
-  const uint8_t* src;      // global chunk, or nullptr: nothing to stream
+  const uint8_t* src;      // global chunk (the last block streams a copy of itself)
+  int wave;                // wave index in the workgroup (uniform)
 };
 
 template <int BYTES>
 __device__ __forceinline__ void stream_piece(const ChunkStream& cs, int r) {
   constexpr int n16 = BYTES / 16;
-  if (!cs.src || r * 256 >= n16) return;
-  const int wave = threadIdx.x >> 6;
-  const int i = threadIdx.x + 256 * r;
-  if (256 * r + 64 * wave < n16)          // whole waves: n16 is a multiple of 64
-    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(cs.src + 16 * (size_t)i),
-                                     (__attribute__((address_space(3))) void*)(cs.dst + 4096 * r + 1024 * wave), 16, 0,
-                                     0);
+  if (r * 256 >= n16) return;
+  // every piece but possibly the last covers all four waves (n16 is a
+  // multiple of 64); the conditions are uniform, so no lane masking
+  if (256 * (r + 1) > n16 && 256 * r + 64 * cs.wave >= n16) return;
+  __builtin_amdgcn_global_load_lds(
+      (const __attribute__((address_space(1))) void*)(cs.src + 4096 * r + 1024 * cs.wave + 16 * (threadIdx.x & 63)),
+      (__attribute__((address_space(3))) void*)(cs.dst + 4096 * r + 1024 * cs.wave), 16, 0, 0);
 }
 
 template <int BYTES>
@@ -102,7 +104,7 @@ __device__ __forceinline__ void stream_pieces_from(const ChunkStream& cs, int r0
 
 template <int BYTES>
 __device__ __forceinline__ void stage_chunk_async(uint8_t* lds, const uint8_t* __restrict__ g) {
-  stream_pieces_from<BYTES>(ChunkStream{lds, g}, 0);
+  stream_pieces_from<BYTES>(ChunkStream{lds, g, __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6))}, 0);
 }
 
 __device__ __forceinline__ void wait_async_copies() { __builtin_amdgcn_s_waitcnt(0x0F70); }   // vmcnt(0)
@@ -640,6 +642,7 @@ __global__ void __launch_bounds__(256, (G == 1 ? 4 : (G == 2 ? 3 : 1))) k_attn_h
   st.inv_rho = 1.0f;
 
   const uint8_t* ws_base = a.ws + ((size_t)(tm.b * a.hkv + tm.hk) * a.NB) * lay.bytes;
+  const int wave_u = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   stage_chunk_async<cbytes>(smem, ws_base);
   wait_async_copies();
   __syncthreads();
@@ -648,7 +651,8 @@ __global__ void __launch_bounds__(256, (G == 1 ? 4 : (G == 2 ? 3 : 1))) k_attn_h
     set_priority_by_work_left(tm.nJ - J);
     const uint8_t* cur = smem + (J & 1) * cbytes;
     // chunk J+1 streams into the other buffer while block J is processed
-    const ChunkStream cs{smem + ((J + 1) & 1) * cbytes, J + 1 < tm.nJ ? ws_base + (size_t)(J + 1) * cbytes : nullptr};
+    const ChunkStream cs{smem + ((J + 1) & 1) * cbytes, ws_base + (size_t)(J + 1 < tm.nJ ? J + 1 : J) * cbytes,
+                         wave_u};
     if (J < jw_last)
       hif4_block<G, NORM, DEBUG, false>(a, tm, cur, J, lane, h, col, qi, row_ok, qop, bq, ones, st, cs);
     else if (J == jw_last)

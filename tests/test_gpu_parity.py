@@ -85,13 +85,19 @@ def test_quantize_v_bitexact(h):
     assert np.array_equal(to_np(g[1]).view(np.uint32), meta)
 
 
-def _run_and_compare(h, q, k, v, cu, s, max_seqlen, norm="preorder", heads=None, rows=None, check_p=True):
+def _run_and_compare(h, q, k, v, cu, s, max_seqlen, norm="preorder", heads=None, rows=None, check_p=True,
+                     seqs=None):
+    """Runs the HIP forward on the whole problem, the oracle on the sampled
+    (sequence, head, row) set, and compares O, LSE and (check_p) the P^ dump.
+    Only the sampled slices of the GPU outputs are copied to the host."""
+    import torch
     cu_t = None if cu is None else to_gpu(cu)
     nm = h.NORM_PREORDER if norm == "preorder" else h.NORM_INCONSISTENT
-    o, lse, pc, pm = h.hifa4_attention_fwd(to_gpu(q), to_gpu(k), to_gpu(v), None if s is None else to_gpu(s),
-                                           cu_seqlens=cu_t, max_seqlen=max_seqlen, norm=nm, debug_p=True)
-    o, lse, pc, pm = to_np(o), to_np(lse), to_np(pc), to_np(pm).view(np.uint32)
-    ref = oatt.attention_fwd(q, k, v, s, cu_seqlens=cu, norm=norm, heads=heads, rows=rows, want_p=True)
+    res = h.hifa4_attention_fwd(to_gpu(q), to_gpu(k), to_gpu(v), None if s is None else to_gpu(s),
+                                cu_seqlens=cu_t, max_seqlen=max_seqlen, norm=nm, debug_p=check_p)
+    o, lse = res[0], res[1]
+    ref = oatt.attention_fwd(q, k, v, s, cu_seqlens=cu, norm=norm, heads=heads, rows=rows, want_p=check_p,
+                             seqs=seqs)
     if cu is None:
         bsz, S = q.shape[:2]
         cuv = np.arange(bsz + 1) * S
@@ -101,13 +107,16 @@ def _run_and_compare(h, q, k, v, cu, s, max_seqlen, norm="preorder", heads=None,
     worst = 0.0
     for (b, hh), r in ref.items():
         tok = cuv[b] + r["rows"]
-        worst = max(worst, check_close(o[tok, hh], r["o"], what=f"O seq {b} head {hh}"))
-        check_close(lse[hh, tok], r["lse"], atol=2e-3, rtol=0, what="LSE")
+        tok_t = torch.as_tensor(tok, device=o.device, dtype=torch.long)
+        worst = max(worst, check_close(to_np(o[tok_t, hh]), r["o"], what=f"O seq {b} head {hh}"))
+        check_close(to_np(lse[hh, tok_t]), r["lse"], atol=2e-3, rtol=0, what="LSE")
         if check_p:
+            pc = to_np(res[2][hh, tok_t])
+            pm = to_np(res[3][hh, tok_t]).view(np.uint32)
             for ii, i in enumerate(r["rows"]):
                 nb_i = i // 64 + 1
-                assert np.array_equal(pc[hh, tok[ii], :nb_i], r["p_codes"][ii, :nb_i]), (b, hh, i)
-                assert np.array_equal(pm[hh, tok[ii], :nb_i], r["p_meta"][ii, :nb_i]), (b, hh, i)
+                assert np.array_equal(pc[ii, :nb_i], r["p_codes"][ii, :nb_i]), (b, hh, i)
+                assert np.array_equal(pm[ii, :nb_i], r["p_meta"][ii, :nb_i]), (b, hh, i)
     return worst
 
 
@@ -200,3 +209,49 @@ def test_qwen3_shape_sampled(h):
     rows = [0, 1, 31, 63, 64, 65, 1000, 2047, 2048, 3071, 4031, 4094, 4095]
     _say("qwen3 sampled")
     _run_and_compare(h, q, k, v, None, s, w.seqlen, heads=[0, 3, 4, 17, 31], rows=rows)
+
+
+def test_long_s32768_sampled(h):
+    """Long prefill, S=32768, at full size in the benchmark's launch shape,
+    Smooth-QK scales from the Qwen3-shaped calibration draw: sampled heads and
+    rows (first, block edges, middle, last); O and LSE against the oracle.
+    The P^ dump is not requested here (it would take 17 GB at this length);
+    P^ codes are compared bit for bit on the S=4096 workload."""
+    w = WORKLOADS["long_s32768"]
+    q, k, v, _ = make_inputs(w)
+    qc, kc = make_calibration(WORKLOADS[w.calib_from], n=4)
+    s, _ = osmooth.calibrate(qc, kc, w.heads_kv, w.alpha)
+    rows = [0, 63, 64, 4097, 16383, 16384, 32700, 32767]
+    _say("long_s32768 sampled")
+    _run_and_compare(h, q, k, v, None, s, w.seqlen, heads=[2, 29], rows=rows, check_p=False)
+
+
+def test_varlen_b16_full(h):
+    """Batched variable-length prefill (16 sequences of 512..2048 tokens,
+    packed with cu_seqlens, Smooth-QK off) at full size: every sequence,
+    sampled heads and rows, P^ codes bit-exact; then the inconsistent
+    normalizer on the same inputs."""
+    w = WORKLOADS["varlen_b16"]
+    q, k, v, cu = make_inputs(w)
+    rows = [0, 1, 63, 64, 300, 511, 1000, 1500, 2047]
+    _say("varlen_b16 preorder")
+    _run_and_compare(h, q, k, v, cu, None, int(w.seqlens().max()), heads=[0, 13, 31], rows=rows)
+    _say("varlen_b16 inconsistent")
+    _run_and_compare(h, q, k, v, cu, None, int(w.seqlens().max()), norm="inconsistent", heads=[5], rows=rows,
+                     check_p=False)
+
+
+def test_wide_d256_sampled(h):
+    """Wide heads (D=256, B=2, S=8192, Smooth-QK on) at full size: sampled
+    sequences, heads and rows, P^ codes bit-exact; the inconsistent
+    normalizer's O and LSE against the oracle's."""
+    w = WORKLOADS["wide_d256"]
+    q, k, v, _ = make_inputs(w)
+    qc, kc = make_calibration(w, n=2, seqlen=2048)
+    s, _ = osmooth.calibrate(qc, kc, w.heads_kv, w.alpha)
+    rows = [0, 64, 2047, 4096, 8191]
+    _say("wide_d256 preorder")
+    _run_and_compare(h, q, k, v, None, s, w.seqlen, heads=[1, 14], rows=rows, seqs=[0, 1])
+    _say("wide_d256 inconsistent")
+    _run_and_compare(h, q, k, v, None, s, w.seqlen, norm="inconsistent", heads=[6], rows=rows, seqs=[1],
+                     check_p=False)
