@@ -80,6 +80,66 @@ def cpu_baseline(w, q, k, v, s, n_heads):
                       f"= cores)"}
 
 
+def config_report(h, torch, np, name, ws):
+    """Throughput of the HiFA4 forward on another workload (inputs resident,
+    Smooth-QK scales from its calibration draw via the GPU calibration call);
+    for the wide-head workload also the inconsistent normalizer and its eps,
+    on the GPU and from the oracle on sampled rows."""
+    from paper_2607_04302_amd.workloads import WORKLOADS, make_calibration, make_inputs
+    w = WORKLOADS[name]
+    dev = torch.device("cuda:0")
+    qn, kn, vn, cun = make_inputs(w)
+    q, k, v = (torch.from_numpy(x).to(dev) for x in (qn, kn, vn))
+    cu = None if cun is None else torch.from_numpy(cun).to(dev)
+    s = sn = None
+    if w.alpha > 0:
+        src = WORKLOADS[w.calib_from] if w.calib_from else w
+        qc, kc = make_calibration(src)
+        s, _ = h.hifa4_calibrate_smooth_qk(torch.from_numpy(qc).to(dev), torch.from_numpy(kc).to(dev), w.alpha)
+        sn = s.cpu().numpy()
+        del qc, kc
+    flops = w.flops()
+    max_s = int(w.seqlens().max())
+    steps = max(3, min(50, int(2e12 / flops)))
+    kw = dict(cu_seqlens=cu, max_seqlen=max_s, workspace=ws)
+
+    def run(norm, n):
+        for _ in range(2):
+            h.hifa4_attention_fwd(q, k, v, s, norm=norm, **kw)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(n):
+            res = h.hifa4_attention_fwd(q, k, v, s, norm=norm, **kw)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e3 / n, res
+
+    ms, (o, lse) = run(h.NORM_PREORDER, steps)
+    tf = flops / (ms * 1e-3) / 1e12
+    out = {"workload": name, "batch": w.batch, "heads_q": w.heads_q, "heads_kv": w.heads_kv, "head_dim": w.head_dim,
+           "seqlen": (f"{w.varlen_range[0]}..{w.varlen_range[1]}" if w.varlen else w.seqlen),
+           "smooth_qk": s is not None, "gflop_per_step": round(flops / 1e9, 3), "steps": steps,
+           "ms_per_step": round(ms, 4), "value": round(tf, 2), "unit": "TFLOP/s",
+           "pct_fp4_peak": round(100.0 * tf / PEAK_FP6_TFLOPS, 3)}
+    if name == "wide_d256":
+        msi, (oi, lsei) = run(h.NORM_INCONSISTENT, steps)
+        eps = torch.expm1(lse.double() - lsei.double()).cpu().numpy()
+        from oracle import attention as oatt
+        rows = [64, 2047, 4096, 8191]
+        heads = [3]
+        rc = oatt.attention_fwd(qn, kn, vn, sn, heads=heads, rows=rows, seqs=[0])
+        rm = oatt.attention_fwd(qn, kn, vn, sn, heads=heads, rows=rows, seqs=[0], norm="inconsistent")
+        eps_o = np.expm1(rc[(0, 3)]["lse"] - rm[(0, 3)]["lse"])
+        eps_g = eps[3, rows]
+        out["inconsistent_variant"] = {
+            "ms_per_step": round(msi, 4), "eps_row_median": float(np.median(eps)),
+            "eps_row_frac_negative": float((eps < 0).mean()),
+            "eps_sampled_rows": {"rows": rows, "head": 3, "gpu": [float(x) for x in eps_g],
+                                 "oracle": [float(x) for x in eps_o]}}
+    del q, k, v, o, lse
+    torch.cuda.empty_cache()
+    return out
+
+
 def time_variant(h, torch, args, q, k, v, s, norm, operands, steps, warmup, ws):
     """Run warmup + steps back-to-back calls; returns (ms_per_step wall,
     per-step prepass ms, per-step attention ms) with HIP events recorded by the
@@ -115,6 +175,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-variants", action="store_true", help="time only the HiFA4 path")
     ap.add_argument("--cpu-heads", type=int, default=8)
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the throughput of the other workloads (tiny, long, varlen, wide)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB five times (the reference kernel that "
                          "scales HBM traffic counters) and exit")
@@ -217,6 +279,11 @@ def main():
         diff = (out.float() - out16.float()).norm() / out16.float().norm()
         result["rel_l2_vs_fp16_variant"] = round(float(diff), 5)
         del out16, outi, lsei
+    if not args.no_configs:
+        del out, lse
+        torch.cuda.empty_cache()
+        result["other_configs"] = [config_report(h, torch, np, name, ws)
+                                   for name in ("tiny_s256", "long_s32768", "varlen_b16", "wide_d256")]
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, qn, kn, vn, sn, args.cpu_heads)
     print(json.dumps(result), flush=True)
