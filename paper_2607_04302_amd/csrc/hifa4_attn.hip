@@ -12,19 +12,22 @@
 // key blocks first).
 //
 // Per 64-key block (one P group, one V group) and wave:
-//   S^T[key, q] = K^ Q^T with 32x32x64 FP6 MFMAs per 64-channel group
-//     (the A operand is the pre-pass K tile in LDS, B the Q tile quantized in
-//     registers at kernel start); each MFMA sum is exact, the fp32 epilogue
-//     applies b_Q*b_K per group and sums the groups in order, then x c and to
-//     fp16.  In S^T each lane holds one query and 32 of the block's keys, so
-//     row maxima are in-lane plus one exchange with lane l^32;
+//   S^T[key, q] = K^ Q^T with two 32x32x64 FP6 MFMAs per 64-channel group
+//     and 32-key half (the A operands are the pre-pass K records in LDS, whose
+//     E8M0 scales carry b_K exactly; B is the Q tile quantized in registers at
+//     kernel start); each group sum is exact, the fp32 epilogue applies b_Q
+//     per group and sums the groups in order, then x c, then to fp16.  In S^T
+//     each lane holds one query and 32 of the block's keys, so row maxima are
+//     in-lane plus one exchange with lane l^32;
 //   FP16 softmax: m_new = max(m, rowmax), P = 2^(S2 - m_new), r = 2^(m - m_new);
 //   P^ = HIF4(P) in registers: the lane's 32 keys are 8 complete 4-key blocks,
 //     8-key blocks pair with lane l^32; values become FP6 operands directly;
 //   O^T[d, q] += V^T P^T: the lane's P^ values already form the B operand of
-//     the 32x32x64 MFMA (the pre-pass stored V^ in the matching key order), an
-//     fp32 epilogue applies b_P*b_V; the normalizer comes out of one more
-//     MFMA against an all-ones A operand (the [V^ | 1] column of the paper).
+//     the 32x32x64 MFMA (the pre-pass stored V^ in the matching key order, as
+//     two operands per group whose scales carry b_V), an fp32 epilogue
+//     applies b_P and the deferred rescale; the normalizer comes out of one
+//     more MFMA against an all-ones A operand (the [V^ | 1] column of the
+//     paper).
 #include "hifa4_device.h"
 #include "hifa4_internal.h"
 
@@ -74,8 +77,9 @@ __device__ __forceinline__ void stage_chunk(uint8_t* lds, const uint8_t* __restr
 // memory straight into LDS (global_load_lds, 16 bytes per lane; lane i of a
 // wave lands at the wave's LDS base + 16 i), in pieces of 256 lanes x 16
 // bytes.  On the last block of a tile the current chunk is streamed into the
-// idle buffer again, which keeps the block code free of branches.  Completion is tracked by vmcnt: the caller waits with vmcnt(0) and
-// a barrier before reading.  Issuing a piece stalls the wave while the
+// idle buffer again, which keeps the block code free of branches.
+// Completion is tracked by vmcnt: the caller waits with vmcnt(0) and a
+// barrier before reading.  Issuing a piece stalls the wave while the
 // texture path is busy, so the block code spreads the pieces over its phases
 // instead of issuing the whole chunk at once.
 struct ChunkStream {
@@ -218,11 +222,12 @@ __device__ __forceinline__ int key_of(int t, int h, int v) { return 32 * t + 8 *
 // HiFA4 kernel.
 //
 // K/V chunks alternate between two LDS buffers: while block J is consumed,
-// chunk J+1 is fetched into registers and stored to the other buffer before
-// the block's closing barrier.  Two waves per SIMD let one wave's MFMAs run
-// under the other's vector work.  The block that holds a wave's diagonal is
-// processed by a separate instantiation (MASK) so that the causal mask costs
-// nothing on the other blocks.
+// chunk J+1 streams into the other buffer (global_load_lds), and the block's
+// closing barrier waits for it.  At D=128 three waves per SIMD (three
+// workgroups per CU) let one wave's MFMAs and memory waits run under the
+// others' vector work.  The block that holds a wave's diagonal is processed by
+// a separate instantiation (MASK) so that the causal mask costs nothing on the
+// other blocks.
 //
 // Scores: for each 32-key half t and channel group g two MFMAs accumulate
 // K^'s codes and the second operand of the split base (zero, the codes or the
