@@ -8,6 +8,9 @@ resident in HBM.  Prints one JSON line.
 
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--gpus 1]
 
+Before the warm-up steps the forward runs untimed for 0.3 s so that the GPU
+reaches steady clocks (a cold MI355X needs ~40 ms of sustained work).
+
 The line carries the metric (effective attention TFLOP/s over causal pairs),
 the fraction of the dense FP4/FP6 MFMA peak, the in-run FP16-operand variant,
 the roofline of the dominant kernel (measured with HIP events on the launch
@@ -140,6 +143,23 @@ def config_report(h, torch, np, name, ws):
     return out
 
 
+def settle_clocks(h, torch, q, k, v, s, ws, seconds=0.3):
+    """Untimed calls of the measured forward until the GPU has run it for
+    `seconds` of wall time.  A cold MI355X raises its clocks over the first
+    ~40 ms of sustained work (a call at S=4096 takes ~1.3x its steady-state
+    time at first), so the timed steps start from steady clocks whatever the
+    warm-up count.  Returns the number of calls."""
+    n = 0
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(10):
+            h.hifa4_attention_fwd(q, k, v, s, workspace=ws)
+        torch.cuda.synchronize()
+        n += 10
+    return n
+
+
 def time_variant(h, torch, args, q, k, v, s, norm, operands, steps, warmup, ws):
     """Run warmup + steps back-to-back calls; returns (ms_per_step wall,
     per-step prepass ms, per-step attention ms) with HIP events recorded by the
@@ -169,8 +189,8 @@ def time_variant(h, torch, args, q, k, v, s, norm, operands, steps, warmup, ws):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="qwen3_8b_s4096")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-variants", action="store_true", help="time only the HiFA4 path")
@@ -230,6 +250,7 @@ def main():
     flops = w.flops()
     ws = h.Workspace()
 
+    settle = settle_clocks(h, torch, q, k, v, s, ws)
     wall, pre_ms, att_ms, out, lse = time_variant(h, torch, args, q, k, v, s, h.NORM_PREORDER, h.OPERANDS_HIF4,
                                                   args.steps, args.warmup, ws)
     value = flops / (wall * 1e-3) / 1e12
@@ -259,6 +280,7 @@ def main():
                      "traffic": traffic, "kernel": f"k_attn_hif4<G={w.head_dim // 64},preorder>",
                      "source_sha256": source_digest()},
         "paper_context": PAPER_CONTEXT,
+        "clock_settle_calls": settle,
     }
     if not args.no_variants:
         wall16, pre16, att16, out16, _ = time_variant(h, torch, args, q, k, v, None, h.NORM_PREORDER,
