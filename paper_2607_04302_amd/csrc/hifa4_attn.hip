@@ -565,6 +565,10 @@ __global__ void __launch_bounds__(256, (G == 1 ? 4 : (G == 2 ? 3 : 1))) k_attn_h
   const int qi = tm.qw + col;
   const bool row_ok = tm.active && qi < tm.L;
   const int jw_last = tm.active ? (min(tm.qw + 31, tm.L - 1)) / 64 : -1;
+  // the first K/V chunk streams into LDS while the Q tile is loaded and quantized
+  const uint8_t* ws_base = a.ws + ((size_t)(tm.b * a.hkv + tm.hk) * a.NB) * lay.bytes;
+  const int wave_u = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  stage_chunk_async<cbytes>(smem, ws_base);
 
   // ---- Q tile: Smooth-QK (fp16(q*s)) then HIF4 into FP6 B operands.
   i8_t qop[G];
@@ -646,9 +650,6 @@ __global__ void __launch_bounds__(256, (G == 1 ? 4 : (G == 2 ? 3 : 1))) k_attn_h
   st.l_star = 0.0f;
   st.inv_rho = 1.0f;
 
-  const uint8_t* ws_base = a.ws + ((size_t)(tm.b * a.hkv + tm.hk) * a.NB) * lay.bytes;
-  const int wave_u = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
-  stage_chunk_async<cbytes>(smem, ws_base);
   wait_async_copies();
   __syncthreads();
 
