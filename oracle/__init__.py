@@ -11,6 +11,7 @@ Modules
   softmax16   the FP16 softmax exponential E(x) (Appendix C, FP16 operations)
   smooth      Smooth-QK calibration, gate and application (Eq. 1, Sections 4.2-4.4)
   attention   the C4V16 tiled forward with P-Reordering (Algorithm 1, Thm. 1)
+  qmean       the Q-Mean auxiliary (Algorithm 1, mu step; Section 4.6; App. C)
 
 Parity status: every function here is pinned by a ``-m "not gpu"`` test against
 something other than itself (exhaustive exact enumeration, closed forms from

@@ -1,6 +1,7 @@
 """The HiFA4 (C4V16) causal prefill forward, step by step.
 
-Paper: Algorithm 1 (C4V16-Aux), without the Q-Mean steps; Background,
+Paper: Algorithm 1 (C4V16-Aux), with the Q-Mean steps optional (qmean.py);
+Background,
 "FlashAttention tiling" (online softmax); Section 4.5 (P-Reordering,
 Theorem 1, fused normalizer [V|1]); "P-Reordering under online softmax";
 Appendix C (quantized tensors, FP16 operations, GQA).
@@ -39,6 +40,7 @@ import numpy as np
 
 from . import hif4
 from .smooth import apply as smooth_apply
+from .qmean import correction, key_sums, token_mean, zero_mean
 from .softmax16 import exp2_fp16, sub_fp16
 
 BLOCK = 64
@@ -71,15 +73,16 @@ def quantize_tokens(v):
     return f, vhat
 
 
-def scores_hif4(qhat, khat, head_dim):
+def scores_hif4(qhat, khat, head_dim, corr=None):
     """S2 = fp16(fp32(S_acc * c)) from dequantized operands (float64 [n, D]
     and [L, D]).  Each group dot is exact in float64 (integer grid, at most 22
     significant bits) and in fp32; the fp32 partial sums round to nearest; the
     scaled score S_acc * c is rounded to fp32 and then to fp16 (both round to
     nearest even): the scores are scaled in the fp32 accumulator precision and
-    handed to the FP16 softmax."""
+    handed to the FP16 softmax.  With Q-Mean, corr [n, L] (fp32) is the
+    accumulator's first term."""
     c = score_scale(head_dim)
-    s_acc = None
+    s_acc = None if corr is None else np.asarray(corr, np.float32)
     for g in range(head_dim // 64):
         sl = slice(64 * g, 64 * g + 64)
         t = (qhat[:, sl] @ khat[:, sl].T).astype(np.float32)   # exact
@@ -155,12 +158,13 @@ def _as_varlen(q, k, v, cu_seqlens):
 
 
 def attention_fwd(q, k, v, s=None, cu_seqlens=None, norm="preorder", operands="hif4",
-                  heads=None, seqs=None, rows=None, want_p=False, arith="contract"):
+                  heads=None, seqs=None, rows=None, want_p=False, arith="contract", q_mean=False):
     """HiFA4 forward on fp16 inputs.
 
     q [B,S,Hq,D] (or [T,Hq,D] with cu_seqlens), k/v [.., Hkv, D], s fp32
     [Hkv, D] or None (no smoothing).  ``heads``/``seqs``/``rows`` restrict the
     computation to a sample (rows are positions within each sequence).
+    ``q_mean`` adds the Q-Mean auxiliary (HIF4 operands only).
     Returns a dict keyed by (seq, head) with o (float64 O/l), o16, lse, and,
     with want_p, the canonical P^ codes/metadata per (row, block)."""
     qv, kv, vv, cu = _as_varlen(q, k, v, cu_seqlens)
@@ -178,15 +182,27 @@ def attention_fwd(q, k, v, s=None, cu_seqlens=None, norm="preorder", operands="h
             hk = h // grp
             qs, ks, vs = qv[t0:t1, h], kv[t0:t1, hk], vv[t0:t1, hk]
             if arith == "exact":
-                s2 = (qs.astype(np.float64)[rr] @ ks.astype(np.float64).T) * (math.log2(math.e) / math.sqrt(d))
+                q64, k64 = qs.astype(np.float64)[rr], ks.astype(np.float64)
+                if q_mean:
+                    mu = q64.mean(axis=1)
+                    s_raw = (q64 - mu[:, None]) @ k64.T + mu[:, None] * k64.sum(axis=1)[None, :]
+                else:
+                    s_raw = q64 @ k64.T
+                s2 = s_raw * (math.log2(math.e) / math.sqrt(d))
                 vop = np.zeros((-(-length // BLOCK) * BLOCK, d)); vop[:length] = vs
                 res = online_softmax(s2, vop, rr, length, False, arith="exact")
             elif operands == "hif4":
-                qhat = quantize_rows(qs[rr])["xhat"].reshape(len(rr), d)
+                corr = None
+                if q_mean:
+                    mu = token_mean(qs[rr])
+                    qhat = quantize_rows(zero_mean(qs[rr], mu))["xhat"].reshape(len(rr), d)
+                    corr = correction(mu, key_sums(ks))
+                else:
+                    qhat = quantize_rows(qs[rr])["xhat"].reshape(len(rr), d)
                 khat = quantize_rows(ks)["xhat"].reshape(length, d)
                 if hk not in vcache:
                     vcache[hk] = quantize_tokens(vs)[1]
-                s2 = scores_hif4(qhat, khat, d)
+                s2 = scores_hif4(qhat, khat, d, corr)
                 res = online_softmax(s2, vcache[hk], rr, length, True, want_p=want_p)
             else:
                 s2 = scores_fp16(qs[rr], ks, d)
@@ -211,6 +227,18 @@ def quantize_qk(q, k, s=None):
     qc, qm = hif4.pack(quantize_rows(q))
     kc, km = hif4.pack(quantize_rows(k))
     return qc, qm, kc, km
+
+
+def quantize_q_mean(q, k, s=None):
+    """Q-Mean quantities after Smooth-QK: mu [..., Hq] fp16, kappa [..., Hkv]
+    fp32, and HIF4 of Q_z = Q~ - mu in the canonical layout (codes
+    [..., Hq, D/64, 32], meta [..., Hq, D/64]).  K^ is that of quantize_qk."""
+    hkv = k.shape[-2]
+    if s is not None:
+        q, k = smooth_apply(q, k, s, hkv)
+    mu = token_mean(q)
+    qc, qm = hif4.pack(quantize_rows(zero_mean(q, mu)))
+    return mu, key_sums(k), qc, qm
 
 
 def quantize_v(v, cu_seqlens=None):

@@ -1,0 +1,55 @@
+"""Q-Mean auxiliary (Algorithm 1, the mu step and the score correction;
+Section 4.6; Appendix C, "Q-Mean GEMV and coordinate consistency").
+
+Test infrastructure: only the tests, the smoke check and the benchmark's CPU
+baseline use this package.
+
+The mean of each smoothed query row over the head dimension is removed before
+HIF4 quantization, and the scores get the product of that mean with the sum
+of the smoothed key's channels back, so that in exact arithmetic
+Q_z K~^T + mu * sum_c K~ = Q~ K~^T.  Both sums run over the channels of one
+(token, head) row; the correction uses the smoothed key K~ (the coordinate
+frame of the quantized product), not K.
+
+Readings fixed here (the paper names the operation but not its rounding):
+  * mu_i = fp16(sum_c q~_ic / D): the sum of the fp16 values is exact (float64
+    holds any sum of at most 2^11 fp16 values exactly) and the quotient is
+    rounded once to fp16 (mu is an FP16 quantity of the GEMV);
+  * Q_z = fp16(q~ - mu): the exact difference rounded once;
+  * kappa_j = fp32(sum_c k~_jc): the exact sum rounded once to fp32;
+  * the correction enters the fp32 score accumulator first:
+    corr = fp32(mu_i * kappa_j),
+    S_acc = fp32(...fp32(fp32(corr + t_0) + t_1)... + t_{G-1}) with t_g the
+    exact per-group HIF4 dots; then S2 = fp16(fp32(S_acc * c)) as without
+    Q-Mean.  Algorithm 1 writes the correction after the division by sqrt(d);
+    it is scaled with the rest of S here, which is what the identity above
+    requires.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+
+def token_mean(q_tilde):
+    """mu = fp16(exact sum over the last axis / D) of fp16 values."""
+    x = np.asarray(q_tilde, np.float16).astype(np.float64)
+    return (x.sum(axis=-1) / x.shape[-1]).astype(np.float16)
+
+
+def zero_mean(q_tilde, mu):
+    """Q_z = fp16(q~ - mu), mu broadcast over the last axis."""
+    a = np.asarray(q_tilde, np.float16).astype(np.float64)
+    b = np.asarray(mu, np.float16).astype(np.float64)[..., None]
+    return (a - b).astype(np.float16)
+
+
+def key_sums(k_tilde):
+    """kappa = fp32(exact sum over the last axis) of fp16 values."""
+    return np.asarray(k_tilde, np.float16).astype(np.float64).sum(axis=-1).astype(np.float32)
+
+
+def correction(mu, kappa):
+    """corr[i, j] = fp32(mu_i * kappa_j); the product of an fp16 and an fp32
+    value is exact in float64."""
+    return (np.asarray(mu, np.float16).astype(np.float64)[:, None]
+            * np.asarray(kappa, np.float32).astype(np.float64)[None, :]).astype(np.float32)

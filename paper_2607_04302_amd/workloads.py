@@ -41,6 +41,7 @@ class Workload:
     varlen_range: tuple = (512, 2048)
     calib_seqlen: Optional[int] = None
     calib_from: Optional[str] = None        # reuse another workload's scales
+    q_bias: float = 0.0                     # constant added to every Q element
 
     @property
     def varlen(self) -> bool:
@@ -98,6 +99,8 @@ WORKLOADS = {
 
 def _draw(rng, shape_q, shape_kv, w: Workload):
     q = rng.standard_normal(shape_q, dtype=np.float32)
+    if w.q_bias:
+        q += np.float32(w.q_bias)
     k = rng.standard_normal(shape_kv, dtype=np.float32)
     v = rng.standard_normal(shape_kv, dtype=np.float32)
     ch = w.outlier_channels()
@@ -136,11 +139,12 @@ def make_calibration(w: Workload, n: Optional[int] = None, seqlen: Optional[int]
 
 
 def small_case(heads_q=2, heads_kv=1, head_dim=128, seqlens=(200,), seed=7,
-               outlier_channels=(5, 77), outlier_scale=16.0):
-    """A small seeded case for parity tests (varlen layout if several lengths)."""
+               outlier_channels=(5, 77), outlier_scale=16.0, q_bias=0.0):
+    """A small seeded case for parity tests (varlen layout if several lengths).
+    q_bias shifts every Q element (a DC bias of the queries)."""
     w = Workload("small", len(seqlens), heads_q, heads_kv, head_dim, max(seqlens),
                  outlier_fixed=tuple(c % head_dim for c in outlier_channels) if outlier_channels else (),
-                 outlier_scale=outlier_scale)
+                 outlier_scale=outlier_scale, q_bias=q_bias)
     rng = np.random.default_rng(seed)
     t = int(sum(seqlens))
     q, k, v = _draw(rng, (t, heads_q, head_dim), (t, heads_kv, head_dim), w)
