@@ -13,12 +13,15 @@ Readings fixed here (the paper is silent on them):
     V along tokens (64 tokens of one channel; a partial last group is zero
     padded), P along the 64 keys of a block -- every group lies along the
     contraction axis of its GEMM;
-  * scores: per 64-channel group g the dot t_g of the dequantized operands is
-    exact; S_acc = (((t_0 + t_1) + t_2) + ...) with fp32 round-to-nearest
-    additions; S2 = fp16(fp32(S_acc * c)): the product is rounded to fp32,
-    then to fp16 (both to nearest even), with c = fp32(log2(e)/sqrt(D)), so
-    the softmax runs in base 2
-    (2^(S2-m) equals exp(S/sqrt(D) - m') exactly in real arithmetic);
+  * scores: the softmax scale c = fp32(log2(e)/sqrt(D)) is folded into each
+    query group's scale, w_g = fp32(b_Q,g/4 * c) (b_Q,g the group's E6M2
+    base); per 64-channel group g the dot d_g of the Q operand values
+    (+-u*2^-sh, the dequantized values divided by b_Q,g/4) with the
+    dequantized K^ is exact; the fp32 accumulator takes fp32(d_0 * w_0), then
+    one fused multiply-add d_g * w_g + acc per further group (each rounded
+    once to fp32, nearest even), and S2 = fp16(acc) (nearest even).  The
+    softmax runs in base 2 (2^(S2-m) equals exp(S/sqrt(D) - m') exactly in
+    real arithmetic);
   * running max m and the weights are fp16: m_new = max(m, rowmax S2),
     x = fp16(S2 - m_new), P16 = E(x), r = E(fp16(m - m_new));
   * P-Reordering: P^ = HIF4(P16 over the block), O <- r*O + P^ V^,
@@ -40,6 +43,7 @@ import numpy as np
 
 from . import hif4
 from .smooth import apply as smooth_apply
+from .fparith import fma_f32
 from .qmean import correction, key_sums, token_mean, zero_mean
 from .softmax16 import exp2_fp16, sub_fp16
 
@@ -73,21 +77,40 @@ def quantize_tokens(v):
     return f, vhat
 
 
-def scores_hif4(qhat, khat, head_dim, corr=None):
-    """S2 = fp16(fp32(S_acc * c)) from dequantized operands (float64 [n, D]
-    and [L, D]).  Each group dot is exact in float64 (integer grid, at most 22
-    significant bits) and in fp32; the fp32 partial sums round to nearest; the
-    scaled score S_acc * c is rounded to fp32 and then to fp16 (both round to
-    nearest even): the scores are scaled in the fp32 accumulator precision and
-    handed to the FP16 softmax.  With Q-Mean, corr [n, L] (fp32) is the
-    accumulator's first term."""
+def unit_operands(fields):
+    """The Q operand values +-u*2^-sh of HIF4 groups: the dequantized values
+    divided by b/4 (exact), from the stored fields."""
+    shift = (np.repeat(fields["e2"], 8, axis=-1).astype(np.int64)
+             + np.repeat(fields["e3"], 4, axis=-1))
+    u = fields["u"].astype(np.float64)
+    return np.where(fields["sign"], -u, u) * np.exp2(-shift.astype(np.float64))
+
+
+def scores_hif4(q_op, q_base, khat, head_dim, corr=None):
+    """S2 [n, L] (fp16) from the Q operand values q_op [n, D] (+-u*2^-sh),
+    the Q group bases q_base [n, D/64] (E6M2 values) and the dequantized K^
+    [L, D] (float64).
+
+    w_g = fp32(q_base/4 * c): the exact product rounded once.  Each group dot
+    d_g is exact in float64 and representable in fp32 (integer grid, at most
+    22 significant bits).  acc = fp32(d_0 * w_0) (the exact product rounded
+    once), then acc = fma32(d_g, w_g, acc) for g = 1, 2, ...; S2 = fp16(acc).
+    With Q-Mean, corr [n, L] (fp32, already scaled by c) is the accumulator's
+    starting value and the first group is fused onto it as well."""
     c = score_scale(head_dim)
-    s_acc = None if corr is None else np.asarray(corr, np.float32)
+    w = (np.asarray(q_base, np.float64) / 4.0 * np.float64(c)).astype(np.float32)
+    acc = None if corr is None else np.asarray(corr, np.float32)
     for g in range(head_dim // 64):
         sl = slice(64 * g, 64 * g + 64)
-        t = (qhat[:, sl] @ khat[:, sl].T).astype(np.float32)   # exact
-        s_acc = t if s_acc is None else (s_acc + t)             # fp32 RN add
-    return (s_acc * c).astype(np.float32).astype(np.float16)
+        d = q_op[:, sl] @ khat[:, sl].T                       # exact
+        d32 = d.astype(np.float32)
+        assert np.array_equal(d32.astype(np.float64), d), "group dot not exact in fp32"
+        wg = w[:, g:g + 1]
+        if acc is None:
+            acc = (d * wg.astype(np.float64)).astype(np.float32)  # exact product, one rounding
+        else:
+            acc = fma_f32(d32, wg, acc)
+    return acc.astype(np.float16)
 
 
 def scores_fp16(q, k, head_dim):
@@ -195,14 +218,14 @@ def attention_fwd(q, k, v, s=None, cu_seqlens=None, norm="preorder", operands="h
                 corr = None
                 if q_mean:
                     mu = token_mean(qs[rr])
-                    qhat = quantize_rows(zero_mean(qs[rr], mu))["xhat"].reshape(len(rr), d)
-                    corr = correction(mu, key_sums(ks))
+                    qf = quantize_rows(zero_mean(qs[rr], mu))
+                    corr = correction(mu, key_sums(ks), score_scale(d))
                 else:
-                    qhat = quantize_rows(qs[rr])["xhat"].reshape(len(rr), d)
+                    qf = quantize_rows(qs[rr])
                 khat = quantize_rows(ks)["xhat"].reshape(length, d)
                 if hk not in vcache:
                     vcache[hk] = quantize_tokens(vs)[1]
-                s2 = scores_hif4(qhat, khat, d, corr)
+                s2 = scores_hif4(unit_operands(qf).reshape(len(rr), d), qf["scale"], khat, d, corr)
                 res = online_softmax(s2, vcache[hk], rr, length, True, want_p=want_p)
             else:
                 s2 = scores_fp16(qs[rr], ks, d)

@@ -15,8 +15,9 @@
 //   S^T[key, q] = K^ Q^T with two 32x32x64 FP6 MFMAs per 64-channel group
 //     and 32-key half (the A operands are the pre-pass K records in LDS, whose
 //     E8M0 scales carry b_K exactly; B is the Q tile quantized in registers at
-//     kernel start); each group sum is exact, the fp32 epilogue applies b_Q
-//     per group and sums the groups in order, then x c, then to fp16.  In S^T
+//     kernel start); each group sum is exact, the fp32 epilogue applies
+//     fp32(b_Q/4 * c) per group (c the softmax scale) and accumulates the
+//     groups in order with fused multiply-adds, then rounds to fp16.  In S^T
 //     each lane holds one query and 32 of the block's keys, so row maxima are
 //     in-lane plus one exchange with lane l^32;
 //   FP16 softmax: m_new = max(m, rowmax), P = 2^(S2 - m_new), r = 2^(m - m_new);
@@ -234,8 +235,10 @@ __device__ __forceinline__ int key_of(int t, int h, int v) { return 32 * t + 8 *
 // negated codes), with E8M0 row scales that together make K's exact b/4; the
 // result is the exact sum of o_q * (o_k * b_k/4) in fp32.  V^ enters the PV
 // product the same way, so its groups are exact too.  The epilogue
-// multiplies by the lane's own b_q/4 (each lane owns one query in S^T) and adds
-// the groups in order: two VALU operations per score plus the fp16 rounding.
+// multiplies by the lane's own w_g = fp32(b_q/4 * c) (each lane owns one query
+// in S^T; the softmax scale c is folded in) and accumulates the groups in
+// order with fused multiply-adds: G VALU operations per score plus the fp16
+// rounding.
 //
 // Deferred rescale: instead of O <- r*O every block, the kernel keeps
 // O* = O / rho and l* = l / rho with rho the product of the rescale factors so
@@ -330,6 +333,114 @@ __device__ __forceinline__ uint32_t partner_bperm(uint32_t v, int addr) {
   return (uint32_t)__builtin_amdgcn_ds_bpermute(addr, (int)v);
 }
 
+// fp16(x * s) for both halves of x with per-half fp32 scales: the exact
+// product rounded once (v_fma_mix with an fp16 destination).
+__device__ __forceinline__ h2_t smooth_mul2(h2_t x, float s0, float s1) {
+  h2_t y;
+  asm("v_fma_mixlo_f16 %0, %1, %2, 0 op_sel:[0,0,0] op_sel_hi:[1,0,0]\n\t"
+      "v_fma_mixhi_f16 %0, %1, %3, 0 op_sel:[1,0,0] op_sel_hi:[1,0,0]"
+      : "=&v"(y)
+      : "v"(x), "v"(s0), "v"(s1));
+  return y;
+}
+
+// |x| for both halves (max(x, -x); the values are finite).
+__device__ __forceinline__ h2_t habs2(h2_t x) {
+  h2_t y;
+  asm("v_pk_max_f16 %0, %1, %1 neg_lo:[0,1] neg_hi:[0,1]" : "=v"(y) : "v"(x));
+  return y;
+}
+
+// max(a, b) for both halves, written as an instruction (no canonicalization).
+__device__ __forceinline__ h2_t hmax2_q(h2_t a, h2_t b) {
+  h2_t y;
+  asm("v_pk_max_f16 %0, %1, %2" : "=v"(y) : "v"(a), "v"(b));
+  return y;
+}
+
+// HIF4 of one query group of 64 channels held by a lane pair (lane half h
+// holds channels 32h..32h+31, i.e. 4-blocks 8h..8h+7 and 8-blocks
+// 4h..4h+3, so only the group maximum needs the partner lane), Smooth-QK
+// applied first (sp = the lane's 32 scales, or null).  Produces the lane's
+// FP6 B operand (slot s = channel 32h + s, value +-u*2^-sh) and the group's
+// fp32 score weight w = fp32(b/4 * c).  The decisions are those of the
+// P^ quantizer below: packed fp16 maxima, the E6M2 base from the fp32 bits,
+// the shift constants by saturating 16-bit arithmetic, and one fused
+// multiply-add rounding each magnitude onto its grid.  A negative value whose
+// code is 0 becomes -0, which the MFMA treats as 0.
+__device__ __forceinline__ void quantize_q_half_group(const half_t* __restrict__ src, const float* __restrict__ sp,
+                                                      bool row_ok, float c, i8_t& qop, float& wq) {
+  typedef uint32_t u4v_t __attribute__((ext_vector_type(4)));
+  h2_t x[16];
+  if (row_ok) {
+    const u4v_t* p = reinterpret_cast<const u4v_t*>(src);
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const u4v_t w = p[v];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        // copy the element first: bit-casting an ext_vector element in place
+        // makes clang read element 0 for every i
+        const uint32_t wi = w[i];
+        x[4 * v + i] = __builtin_bit_cast(h2_t, wi);
+      }
+    }
+    if (sp) {
+      const float4* s4 = reinterpret_cast<const float4*>(sp);
+#pragma unroll
+      for (int v = 0; v < 8; ++v) {
+        const float4 sv = s4[v];
+        x[2 * v] = smooth_mul2(x[2 * v], sv.x, sv.y);
+        x[2 * v + 1] = smooth_mul2(x[2 * v + 1], sv.z, sv.w);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) x[i] = h2_t{(half_t)0, (half_t)0};
+  }
+  h2_t ax[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) ax[i] = habs2(x[i]);
+  // 4-block k = pairs 2k, 2k+1; a4p[j] = (A4[2j], A4[2j+1]) = 8-block j's halves
+  h2_t a4p[4], a8[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const h2_t m0 = hmax2_q(ax[4 * j], ax[4 * j + 1]);
+    const h2_t m1 = hmax2_q(ax[4 * j + 2], ax[4 * j + 3]);
+    a4p[j] = hmax_pairs(m0, m1);
+    a8[j] = hmax_halves(a4p[j]);
+  }
+  const h2_t lane_max = hmax2_q(hmax2_q(a8[0], a8[1]), hmax2_q(a8[2], a8[3]));
+  const h2_t gmax = max_with_partner(lane_max);
+  const float A = (float)gmax[0];
+  const uint32_t base = e6m2_ceil(A);
+  const float bval = e6m2_value(base);
+  const float R = hif4_rcp_step(base);
+  const h2_t thr = __builtin_bit_cast(h2_t, __builtin_amdgcn_cvt_pkrtz(0.875f * bval, 0.4375f * bval));
+  const h2_t th_h = {thr[0], thr[0]}, th_q = {thr[1], thr[1]};
+  const uint32_t k400 = 0x04000400u, k5e00 = 0x5E005E00u;
+  h32_t ov;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const h2_t cst = grid_consts(a4p[j], a8[j], th_h, th_q, k400, k5e00);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int i = 4 * j + e;                 // pair i belongs to 4-block 2j + e/2
+      const h2_t o = (e >> 1) ? grid_round2<1>(ax[i], R, cst) : grid_round2<0>(ax[i], R, cst);
+      const uint32_t sgn = __builtin_bit_cast(uint32_t, x[i]) & 0x80008000u;
+      const h2_t os = __builtin_bit_cast(h2_t, __builtin_bit_cast(uint32_t, o) | sgn);
+      ov[2 * i] = os[0];
+      ov[2 * i + 1] = os[1];
+    }
+  }
+  const i6_t pk = __builtin_amdgcn_cvt_scalef32_pk32_fp6_f16(ov, 1.0f);
+#pragma unroll
+  for (int i = 0; i < 6; ++i) qop[i] = pk[i];
+  qop[6] = 0;
+  qop[7] = 0;
+  wq = (0.25f * bval) * c;      // b/4 exact, one rounding with c
+}
+
 template <int G>
 struct Hif4State {
   f16v_t O[2 * G];
@@ -341,12 +452,13 @@ struct Hif4State {
 template <int G, int NORM, bool DEBUG, bool MASK>
 __device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm, const uint8_t* cur, int J, int lane,
                                            int h, int col, int qi, bool row_ok, const i8_t (&qop)[G],
-                                           const float (&bq)[G], const i8_t& ones, Hif4State<G>& st,
+                                           const float (&wq)[G], const i8_t& ones, Hif4State<G>& st,
                                            const ChunkStream& cs) {
   constexpr int DT = 2 * G;
   constexpr ChunkLayout lay = chunk_layout_hif4(G);
   constexpr int CB = (int)lay.bytes;
-  // ---- scores: S2 = fp16(fp32((sum_g acc_g * b_q/4) * c)).
+  // ---- scores: S2 = fp16(acc), acc = fp32(d_0 w_0) then fused d_g w_g + acc,
+  // with w_g = fp32(b_q,g/4 * c) (the softmax scale folded into the group scale).
   h2_t s2[2][8];
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
@@ -368,12 +480,12 @@ __device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm,
     float sacc[16];
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      sacc[v] = acc[0][v] * bq[0];
+      sacc[v] = acc[0][v] * wq[0];
 #pragma unroll
-      for (int g = 1; g < G; ++g) sacc[v] = __builtin_fmaf(acc[g][v], bq[g], sacc[v]);
+      for (int g = 1; g < G; ++g) sacc[v] = __builtin_fmaf(acc[g][v], wq[g], sacc[v]);
     }
 #pragma unroll
-    for (int v2 = 0; v2 < 8; ++v2) s2[t][v2] = scale2_to_f16(sacc[2 * v2], sacc[2 * v2 + 1], a.c);
+    for (int v2 = 0; v2 < 8; ++v2) s2[t][v2] = pack2_f16(sacc[2 * v2], sacc[2 * v2 + 1]);
   }
   if (MASK) {
     const half_t ninf = (half_t)(-__builtin_inff());
@@ -572,58 +684,12 @@ __global__ void __launch_bounds__(256, (G == 1 ? 4 : (G == 2 ? 3 : 1))) k_attn_h
 
   // ---- Q tile: Smooth-QK (fp16(q*s)) then HIF4 into FP6 B operands.
   i8_t qop[G];
-  float bq[G];
+  float wq[G];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
-    float x[32];
-    if (row_ok) {
-      const half_t* src = a.q + ((size_t)(tm.t0 + qi) * a.hq + tm.hq) * D + 64 * g + 32 * h;
-      const u4_t* p = reinterpret_cast<const u4_t*>(src);
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const u4_t w = p[v];
-        const h8_t hh = __builtin_bit_cast(h8_t, w);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) x[8 * v + i] = (float)hh[i];
-      }
-      if (a.s) {
-        const float* sp = a.s + (size_t)tm.hk * D + 64 * g + 32 * h;
-#pragma unroll
-        for (int c = 0; c < 32; ++c) x[c] = (float)mul_rn16(x[c], sp[c]);
-      }
-    } else {
-#pragma unroll
-      for (int c = 0; c < 32; ++c) x[c] = 0.0f;
-    }
-    float a4own[8];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      float mm = fabsf(x[4 * k]);
-#pragma unroll
-      for (int i = 1; i < 4; ++i) mm = fmaxf(mm, fabsf(x[4 * k + i]));
-      a4own[k] = mm;
-    }
-    float a4_all[16];
-    gather_a4<kRows>(a4own, a4_all, h);
-    const GroupMeta gm = group_meta(a4_all);
-    const float R = hif4_rcp_step(gm.base);
-    h32_t hv;
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const float C = round_const(block_shift(gm, 8 * h + k));
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float xv = x[4 * k + i];
-        const float ov = hif4_elem(fabsf(xv), R, C);
-        hv[4 * k + i] = (half_t)(xv < 0.0f ? -ov : ov);
-      }
-    }
-    const i6_t pk = __builtin_amdgcn_cvt_scalef32_pk32_fp6_f16(hv, 1.0f);
-#pragma unroll
-    for (int i = 0; i < 6; ++i) qop[g][i] = pk[i];
-    qop[g][6] = 0;
-    qop[g][7] = 0;
-    bq[g] = 0.25f * gm.b;
+    const half_t* src = a.q + ((size_t)(tm.t0 + qi) * a.hq + tm.hq) * D + 64 * g + 32 * h;
+    const float* sp = a.s ? a.s + (size_t)tm.hk * D + 64 * g + 32 * h : nullptr;
+    quantize_q_half_group(src, sp, row_ok, a.c, qop[g], wq[g]);
   }
 
   i8_t ones;
@@ -660,9 +726,9 @@ __global__ void __launch_bounds__(256, (G == 1 ? 4 : (G == 2 ? 3 : 1))) k_attn_h
     const ChunkStream cs{smem + ((J + 1) & 1) * cbytes, ws_base + (size_t)(J + 1 < tm.nJ ? J + 1 : J) * cbytes,
                          wave_u};
     if (J < jw_last)
-      hif4_block<G, NORM, DEBUG, false>(a, tm, cur, J, lane, h, col, qi, row_ok, qop, bq, ones, st, cs);
+      hif4_block<G, NORM, DEBUG, false>(a, tm, cur, J, lane, h, col, qi, row_ok, qop, wq, ones, st, cs);
     else if (J == jw_last)
-      hif4_block<G, NORM, DEBUG, true>(a, tm, cur, J, lane, h, col, qi, row_ok, qop, bq, ones, st, cs);
+      hif4_block<G, NORM, DEBUG, true>(a, tm, cur, J, lane, h, col, qi, row_ok, qop, wq, ones, st, cs);
     else
       stream_pieces_from<cbytes>(cs, 0);
     wait_async_copies();

@@ -121,6 +121,13 @@ __device__ __forceinline__ h2_t scale2_to_f16(float a, float b, float c) {
   return y;
 }
 
+// Pack fp16(a) and fp16(b) (round to nearest even) into one register.
+__device__ __forceinline__ h2_t pack2_f16(float a, float b) {
+  h2_t y;
+  asm("v_cvt_pk_f16_f32 %0, %1, %2" : "=v"(y) : "v"(a), "v"(b));
+  return y;
+}
+
 // Pack fp16(a*c) and fp16(b*c) (each rounded once) into one register.
 __device__ __forceinline__ h2_t mul2_rn16(float a, float b, float c) {
   h2_t y;

@@ -74,9 +74,9 @@ def test_theorem1_single_block():
     res = attention.attention_fwd(q, k, v, None, cu_seqlens=cu, want_p=True)[(0, 0)]
     res_mis = attention.attention_fwd(q, k, v, None, cu_seqlens=cu, norm="inconsistent")[(0, 0)]
     _, vhat = attention.quantize_tokens(v[:, 0])
-    qhat = attention.quantize_rows(q[:, 0])["xhat"].reshape(64, 128)
+    qf = attention.quantize_rows(q[:, 0])
     khat = attention.quantize_rows(k[:, 0])["xhat"].reshape(64, 128)
-    s2 = attention.scores_hif4(qhat, khat, 128)
+    s2 = attention.scores_hif4(attention.unit_operands(qf).reshape(64, 128), qf["scale"], khat, 128)
     checked = 0
     for i in range(8, 64):
         keys = np.arange(i + 1)
@@ -182,21 +182,112 @@ def test_smoothing_preserves_qk_direction():
         assert np.max(np.abs(a - b)) < 2e-2 * np.abs(b).max()
 
 
-def test_score_rounding_goes_through_fp32():
-    """S2 = fp16(fp32(S_acc * c)): the scaled score is rounded to fp32 first.
-    Witness: S_acc = 1.386971354484558 (an fp32 value), D = 64.  The exact
-    product S_acc * c lies above the fp16 midpoint M = 0.2501220703125 of
-    0.25 and 0.250244140625 but rounds to M in fp32; rounding M to nearest
-    even gives 0.25, while a single rounding of the exact product would give
-    0.250244140625."""
+def _rn(x, bits, emin):
+    """x (a Fraction) rounded to the nearest binary float with `bits`
+    significant bits and minimum normal exponent emin (ties to even)."""
     from fractions import Fraction
-    s_acc = np.float32(1.386971354484558)
+    if x == 0:
+        return Fraction(0)
+    sgn = -1 if x < 0 else 1
+    a = abs(x)
+    e = a.numerator.bit_length() - a.denominator.bit_length()
+    if Fraction(2) ** e > a:
+        e -= 1
+    e = max(e, emin)
+    ulp = Fraction(2) ** (e - bits + 1)
+    q, r = divmod(a, ulp)
+    if r * 2 > ulp or (r * 2 == ulp and q % 2 == 1):
+        q += 1
+    return sgn * q * ulp
+
+
+def _rn32(x):
+    return _rn(x, 24, -126)
+
+
+def _rn16(x):
+    return _rn(x, 11, -14)
+
+
+def _one_term(d, head_dim):
+    """q_op/q_base/khat arrays whose group dots are d (one term per group)."""
+    g = len(d)
+    q_op = np.zeros((1, head_dim))
+    khat = np.zeros((1, head_dim))
+    for i, dv in enumerate(d):
+        q_op[0, 64 * i] = 1.0
+        khat[0, 64 * i] = dv
+    return q_op, khat
+
+
+def test_score_rounds_to_fp32_then_fp16():
+    """S2 = fp16(acc), acc an fp32 value.  Witness (D = 64, base 4 so that
+    w = c): d = 1.386971354484558 (an fp32 value); the exact product d*c lies
+    above the fp16 midpoint M = 0.2501220703125 of 0.25 and 0.250244140625 but
+    rounds to M in fp32; M then rounds to the even 0.25, while a single
+    rounding of the exact product would give 0.250244140625."""
+    from fractions import Fraction
+    d = float(np.float32(1.386971354484558))
     c = attention.score_scale(64)
-    mid = Fraction(0.25) + Fraction(1, 2 ** 13)
-    assert Fraction(float(s_acc)) * Fraction(float(c)) > mid          # single rounding -> upper
-    qhat = np.zeros((1, 64))
-    khat = np.zeros((1, 64))
-    qhat[0, 0] = float(s_acc)
-    khat[0, 0] = 1.0
-    s2 = attention.scores_hif4(qhat, khat, 64)
+    exact = Fraction(d) * Fraction(float(c))
+    assert _rn16(exact) == Fraction(0.250244140625) and _rn16(_rn32(exact)) == Fraction(0.25)
+    q_op, khat = _one_term([d], 64)
+    s2 = attention.scores_hif4(q_op, np.array([[4.0]]), khat, 64)
     assert s2.dtype == np.float16 and float(s2[0, 0]) == 0.25
+
+
+def test_score_scale_is_folded_into_the_query_scale():
+    """w = fp32(b/4 * c) is rounded before it multiplies the group dot.
+    Witness (D = 64): b = 1.25, d = 48.6416015625.  fp16(fp32(d * w)) =
+    2.7421875, whereas scaling the exact group term d*b/4 by c afterwards
+    (fp16(fp32(fp32(d*b/4) * c))) gives 2.740234375."""
+    from fractions import Fraction
+    d, b = 48.6416015625, 1.25
+    c = Fraction(float(attention.score_scale(64)))
+    w = _rn32(Fraction(b) / 4 * c)
+    assert _rn16(_rn32(Fraction(d) * w)) == Fraction(2.7421875)
+    assert _rn16(_rn32(_rn32(Fraction(d) * Fraction(b) / 4) * c)) == Fraction(2.740234375)
+    q_op, khat = _one_term([d], 64)
+    s2 = attention.scores_hif4(q_op, np.array([[b]]), khat, 64)
+    assert float(s2[0, 0]) == 2.7421875
+
+
+def test_score_groups_accumulate_by_fused_multiply_add():
+    """acc = fp32(d_0 w_0), then acc = fp32(d_1 w_1 + acc) rounded once.
+    Witness (D = 128): d = (-61.828125, 26.4765625), b = (0.375, 0.875): the
+    fused form gives S2 = -0.0005917549133300781, a separate product and sum
+    -0.000591278076171875.  Swapping the groups' scales also changes S2."""
+    from fractions import Fraction
+    d0, d1, b0, b1 = -61.828125, 26.4765625, 0.375, 0.875
+    c = Fraction(float(attention.score_scale(128)))
+    w0, w1 = _rn32(Fraction(b0) / 4 * c), _rn32(Fraction(b1) / 4 * c)
+    a0 = _rn32(Fraction(d0) * w0)
+    fused = _rn16(_rn32(Fraction(d1) * w1 + a0))
+    split = _rn16(_rn32(_rn32(Fraction(d1) * w1) + a0))
+    assert fused == Fraction(-0.0005917549133300781) and split == Fraction(-0.000591278076171875)
+    q_op, khat = _one_term([d0, d1], 128)
+    s2 = attention.scores_hif4(q_op, np.array([[b0, b1]]), khat, 128)
+    assert Fraction(float(s2[0, 0])) == fused
+    s2x = attention.scores_hif4(q_op, np.array([[b1, b0]]), khat, 128)
+    assert Fraction(float(s2x[0, 0])) != fused
+
+
+def test_scores_on_quantized_operands_match_exact_rounding():
+    """On real quantized rows the oracle's scores equal the exact-rational
+    evaluation of the same recipe (every rounding from its definition)."""
+    from fractions import Fraction
+    q, k, v, cu = small_case(heads_q=1, heads_kv=1, seqlens=(6,), seed=17, head_dim=128)
+    qf = attention.quantize_rows(q[:, 0])
+    khat = attention.quantize_rows(k[:, 0])["xhat"].reshape(6, 128)
+    q_op = attention.unit_operands(qf).reshape(6, 128)
+    s2 = attention.scores_hif4(q_op, qf["scale"], khat, 128)
+    c = Fraction(float(attention.score_scale(128)))
+    for i in range(6):
+        for j in range(6):
+            acc = None
+            for g in range(2):
+                dg = sum(Fraction(float(a)) * Fraction(float(b))
+                         for a, b in zip(q_op[i, 64 * g:64 * g + 64], khat[j, 64 * g:64 * g + 64]))
+                wg = _rn32(Fraction(float(qf["scale"][i, g])) / 4 * c)
+                acc = _rn32(dg * wg) if acc is None else _rn32(dg * wg + acc)
+            assert Fraction(float(s2[i, j])) == _rn16(acc), (i, j)

@@ -58,9 +58,27 @@ def test_correction_product_rounds_once_to_fp32():
     mu = np.array([np.float16(1.0 + 2.0 ** -10)], np.float16)
     kap = np.array([np.float32(1.0 + 2.0 ** -23)], np.float32)
     # exact product 1 + 2^-10 + 2^-23 + 2^-33 rounds to 1 + 2^-10 + 2^-23
-    c = qmean.correction(mu, kap)
+    c = qmean.correction(mu, kap, np.float32(1.0))
     assert c.dtype == np.float32
     assert float(c[0, 0]) == 1.0 + 2.0 ** -10 + 2.0 ** -23
+
+
+def test_correction_scales_the_mean_first():
+    """corr = fp32(fp32(mu*c) * kappa): mu*c is rounded to fp32 before the
+    product with kappa.  Witness (D = 128, c = fp32(log2(e)/sqrt(128))):
+    mu = -0.496826171875, kappa = 12.613357543945312 gives
+    -0.7991066575050354; one rounding of the exact triple product would give
+    -0.7991065979003906."""
+    from fractions import Fraction
+    from tests.test_oracle_attention import _rn32
+    from oracle.attention import score_scale
+    mu = np.array([np.float16(-0.496826171875)], np.float16)
+    kap = np.array([np.float32(12.613357543945312)], np.float32)
+    c = score_scale(128)
+    got = Fraction(float(qmean.correction(mu, kap, c)[0, 0]))
+    f_mu, f_c, f_k = Fraction(float(mu[0])), Fraction(float(c)), Fraction(float(kap[0]))
+    assert got == _rn32(_rn32(f_mu * f_c) * f_k) == Fraction(-0.7991066575050354)
+    assert _rn32(f_mu * f_c * f_k) == Fraction(-0.7991065979003906)
 
 
 def test_dc_shift_leaves_q_codes_unchanged():
@@ -98,7 +116,7 @@ def test_q_mean_removes_the_dc_bias_error(monkeypatch):
         assert e_qm < 0.2 and e_qm < 0.7 * e_plain, (key, e_qm, e_plain)
     # the same check fails for a planted sign or scale mistake in the correction
     good = attention.correction
-    for bad in (lambda mu, ka: -good(mu, ka), lambda mu, ka: good(mu, ka) * np.float32(0.5)):
+    for bad in (lambda mu, ka, c: -good(mu, ka, c), lambda mu, ka, c: good(mu, ka, c) * np.float32(0.5)):
         monkeypatch.setattr(attention, "correction", bad)
         wrong = attention.attention_fwd(q, k, v, None, cu_seqlens=cu, q_mean=True)
         assert min(_rel(wrong[key]["o"], ex[key]["o"]) for key in ex) > 0.3
