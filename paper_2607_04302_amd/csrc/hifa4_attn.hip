@@ -361,17 +361,23 @@ __device__ __forceinline__ h2_t hmax2_q(h2_t a, h2_t b) {
 // HIF4 of one query group of 64 channels held by a lane pair (lane half h
 // holds channels 32h..32h+31, i.e. 4-blocks 8h..8h+7 and 8-blocks
 // 4h..4h+3, so only the group maximum needs the partner lane), Smooth-QK
-// applied first (sp = the lane's 32 scales, or null).  Produces the lane's
+// applied first when `smooth` is set.  Produces the lane's
 // FP6 B operand (slot s = channel 32h + s, value +-u*2^-sh) and the group's
 // fp32 score weight w = fp32(b/4 * c).  The decisions are those of the
 // P^ quantizer below: packed fp16 maxima, the E6M2 base from the fp32 bits,
 // the shift constants by saturating 16-bit arithmetic, and one fused
 // multiply-add rounding each magnitude onto its grid.  A negative value whose
 // code is 0 becomes -0, which the MFMA treats as 0.
-__device__ __forceinline__ void quantize_q_half_group(const half_t* __restrict__ src, const float* __restrict__ sp,
-                                                      bool row_ok, float c, i8_t& qop, float& wq) {
-  typedef uint32_t u4v_t __attribute__((ext_vector_type(4)));
+// Raw inputs of one query half-group: the lane's 32 fp16 values and, with
+// Smooth-QK, its 32 scales.
+struct QRaw {
   h2_t x[16];
+  float4 s[8];
+};
+
+__device__ __forceinline__ void load_q_half_group(const half_t* __restrict__ src, const float* __restrict__ sp,
+                                                  bool row_ok, QRaw& r) {
+  typedef uint32_t u4v_t __attribute__((ext_vector_type(4)));
   if (row_ok) {
     const u4v_t* p = reinterpret_cast<const u4v_t*>(src);
 #pragma unroll
@@ -382,21 +388,30 @@ __device__ __forceinline__ void quantize_q_half_group(const half_t* __restrict__
         // copy the element first: bit-casting an ext_vector element in place
         // makes clang read element 0 for every i
         const uint32_t wi = w[i];
-        x[4 * v + i] = __builtin_bit_cast(h2_t, wi);
-      }
-    }
-    if (sp) {
-      const float4* s4 = reinterpret_cast<const float4*>(sp);
-#pragma unroll
-      for (int v = 0; v < 8; ++v) {
-        const float4 sv = s4[v];
-        x[2 * v] = smooth_mul2(x[2 * v], sv.x, sv.y);
-        x[2 * v + 1] = smooth_mul2(x[2 * v + 1], sv.z, sv.w);
+        r.x[4 * v + i] = __builtin_bit_cast(h2_t, wi);
       }
     }
   } else {
 #pragma unroll
-    for (int i = 0; i < 16; ++i) x[i] = h2_t{(half_t)0, (half_t)0};
+    for (int i = 0; i < 16; ++i) r.x[i] = h2_t{(half_t)0, (half_t)0};
+  }
+  if (sp) {
+    const float4* s4 = reinterpret_cast<const float4*>(sp);
+#pragma unroll
+    for (int v = 0; v < 8; ++v) r.s[v] = s4[v];
+  }
+}
+
+__device__ __forceinline__ void quantize_q_half_group(const QRaw& r, bool smooth, float c, i8_t& qop, float& wq) {
+  h2_t x[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) x[i] = r.x[i];
+  if (smooth) {
+#pragma unroll
+    for (int v = 0; v < 8; ++v) {
+      x[2 * v] = smooth_mul2(x[2 * v], r.s[v].x, r.s[v].y);
+      x[2 * v + 1] = smooth_mul2(x[2 * v + 1], r.s[v].z, r.s[v].w);
+    }
   }
   h2_t ax[16];
 #pragma unroll
@@ -677,20 +692,24 @@ __global__ void __launch_bounds__(256, (G == 1 ? 4 : (G == 2 ? 3 : 1))) k_attn_h
   const int qi = tm.qw + col;
   const bool row_ok = tm.active && qi < tm.L;
   const int jw_last = tm.active ? (min(tm.qw + 31, tm.L - 1)) / 64 : -1;
-  // the first K/V chunk streams into LDS while the Q tile is loaded and quantized
+  // the first K/V chunk streams into LDS while the Q tile is quantized
   const uint8_t* ws_base = a.ws + ((size_t)(tm.b * a.hkv + tm.hk) * a.NB) * lay.bytes;
   const int wave_u = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
-  stage_chunk_async<cbytes>(smem, ws_base);
-
-  // ---- Q tile: Smooth-QK (fp16(q*s)) then HIF4 into FP6 B operands.
-  i8_t qop[G];
-  float wq[G];
+  // ---- Q tile: Smooth-QK (fp16(q*s)) then HIF4 into FP6 B operands.  The
+  // Q rows and scales are requested before the chunk stream, whose
+  // instructions hold the wave while they issue.
+  QRaw raw[G];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
     const half_t* src = a.q + ((size_t)(tm.t0 + qi) * a.hq + tm.hq) * D + 64 * g + 32 * h;
     const float* sp = a.s ? a.s + (size_t)tm.hk * D + 64 * g + 32 * h : nullptr;
-    quantize_q_half_group(src, sp, row_ok, a.c, qop[g], wq[g]);
+    load_q_half_group(src, sp, row_ok, raw[g]);
   }
+  stage_chunk_async<cbytes>(smem, ws_base);
+  i8_t qop[G];
+  float wq[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) quantize_q_half_group(raw[g], a.s != nullptr, a.c, qop[g], wq[g]);
 
   i8_t ones;
   {
