@@ -160,7 +160,7 @@ def settle_clocks(h, torch, q, k, v, s, ws, seconds=0.3):
     return n
 
 
-def time_variant(h, torch, args, q, k, v, s, norm, operands, steps, warmup, ws):
+def time_variant(h, torch, args, q, k, v, s, norm, operands, steps, warmup, ws, q_mean=False):
     """Run warmup + steps back-to-back calls; returns (ms_per_step wall,
     per-step prepass ms, per-step attention ms) with HIP events recorded by the
     library on the launch stream around each kernel."""
@@ -170,7 +170,7 @@ def time_variant(h, torch, args, q, k, v, s, norm, operands, steps, warmup, ws):
             e.record()
     torch.cuda.synchronize()
     kw = dict(s=s, norm=norm, operands=operands, smooth_qk=s is not None and operands == h.OPERANDS_HIF4,
-              workspace=ws)
+              workspace=ws, q_mean=q_mean)
     out = torch.empty_like(q)
     lse = torch.empty((q.shape[2], q.shape[0] * q.shape[1]), dtype=torch.float32, device=q.device)
     for _ in range(warmup):
@@ -194,7 +194,7 @@ def main():
     ap.add_argument("--workload", default="qwen3_8b_s4096")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-variants", action="store_true", help="time only the HiFA4 path")
-    ap.add_argument("--cpu-heads", type=int, default=8)
+    ap.add_argument("--cpu-heads", type=int, default=16)
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the throughput of the other workloads (tiny, long, varlen, wide)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -297,6 +297,12 @@ def main():
         result["inconsistent_variant"] = {"ms_per_step": round(walli, 4),
                                           "eps_row_median": float(np.median(eps)),
                                           "eps_row_frac_negative": float((eps < 0).mean())}
+        wallq, preq, attq, outq, _ = time_variant(h, torch, args, q, k, v, s, h.NORM_PREORDER, h.OPERANDS_HIF4,
+                                                  max(5, args.steps // 5), 2, ws, q_mean=True)
+        result["qmean_variant"] = {"value": round(flops / (wallq * 1e-3) / 1e12, 2), "unit": "TFLOP/s",
+                                   "ms_per_step": round(wallq, 4),
+                                   "kernels_ms": {"kv_prepass": round(preq, 4), "attention": round(attq, 4)}}
+        del outq
         # Fidelity diagnostic (not gating): rel-L2 of HiFA4 O against the FP16 variant.
         diff = (out.float() - out16.float()).norm() / out16.float().norm()
         result["rel_l2_vs_fp16_variant"] = round(float(diff), 5)

@@ -10,8 +10,9 @@
  *   - P-Reordering (Section 4.5, Theorem 1): P is quantized first and the
  *     softmax normalizer is accumulated from that same P^ inside the PV
  *     contraction, through an appended ones block [V^ | 1].
- * Algorithm 1 gives the loop; the Q-Mean auxiliary of its lines for mu is not
- * part of this library.
+ * Algorithm 1 gives the loop, including the optional Q-Mean auxiliary (the
+ * per-token mean of Q~ removed before quantization and added back through the
+ * key sums, Section 4.6 and Appendix C).
  *
  * Conventions (all entry points):
  *   - Tensor pointers are DEVICE pointers owned by the caller; the library
@@ -113,7 +114,14 @@ typedef enum {
  *                  caller) that the call records on `stream` before the K/V
  *                  pre-pass, between the pre-pass and the attention kernel,
  *                  and after the attention kernel -- per-kernel device time
- *                  without a profiler.  The events are not waited on. */
+ *                  without a profiler.  The events are not waited on.
+ *   q_mean         0 or 1: the Q-Mean auxiliary (Algorithm 1; Section 4.6;
+ *                  Appendix C).  Per query row mu = fp16(exact sum of the
+ *                  row's D smoothed values / D); the row is quantized as
+ *                  Q_z = fp16(q~ - mu); per key kappa = fp32(exact sum of the
+ *                  key's smoothed channels); the score accumulator starts from
+ *                  fp32(fp32(mu*c) * kappa).  HIF4 operands only
+ *                  (HIFA4_ERR_UNSUPPORTED with FP16 operands). */
 typedef struct {
   int32_t norm;       /* hifa4_norm      */
   int32_t operands;   /* hifa4_operands  */
@@ -121,6 +129,7 @@ typedef struct {
   void* debug_p_codes;
   void* debug_p_meta;
   void** timing_events;
+  int32_t q_mean;
 } hifa4_fwd_options;
 
 /* Host-side calibration report (Table 1 statistics and the gate decision). */
@@ -188,13 +197,17 @@ hifa4_status hifa4_quantize_qk(const hifa4_problem* p, const void* q, const void
 hifa4_status hifa4_quantize_v(const hifa4_problem* p, const void* v, void* v_codes,
                               void* v_meta, void* stream);
 
-/* The HiFA4 causal prefill forward (Algorithm 1 without Q-Mean; Section 4.5).
+/* The HiFA4 causal prefill forward (Algorithm 1; Section 4.5).
  * q: DEVICE fp16 [.., num_heads_q, head_dim]; k, v: DEVICE fp16
  * [.., num_heads_kv, head_dim]; s: DEVICE fp32 [num_heads_kv, head_dim] (may be
  * NULL when opt->smooth_qk == 0 or operands are FP16).
- * Per query row and 64-key block in ascending order: S2 = fp16(fp32(S*c)),
- * S the exact HIF4 dot summed over 64-channel groups in fp32,
- * c = fp32(log2(e)/sqrt(D)); m_new = max(m, rowmax S2); P = fp16(2^(S2-m_new));
+ * Per query row and 64-key block in ascending order: with c =
+ * fp32(log2(e)/sqrt(D)) and, per 64-channel group g of the query, its E6M2
+ * base b_g and weight w_g = fp32(b_g/4 * c), the exact group dot d_g of the
+ * query's operand values (+-u*2^-sh) with the dequantized keys is
+ * accumulated in fp32 as acc = fp32(d_0*w_0) (with Q-Mean: the fused d_0*w_0
+ * + the correction), then acc = fp32(d_g*w_g + acc) fused, and S2 = fp16(acc);
+ * m_new = max(m, rowmax S2); P = fp16(2^(S2-m_new));
  * r = fp16(2^(m-m_new)); P^ = HIF4(P); O = r*O + P^ V^ and l = r*l + P^ 1
  * (fp32 accumulation); O_out = fp16(O/l), LSE = m*ln2 + ln(l).
  * o: DEVICE fp16, same layout as q.  lse: DEVICE fp32 [num_heads_q, T] (T the

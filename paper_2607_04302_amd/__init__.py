@@ -41,7 +41,7 @@ class Problem(ctypes.Structure):
 class FwdOptions(ctypes.Structure):
     _fields_ = [("norm", ctypes.c_int32), ("operands", ctypes.c_int32), ("smooth_qk", ctypes.c_int32),
                 ("debug_p_codes", ctypes.c_void_p), ("debug_p_meta", ctypes.c_void_p),
-                ("timing_events", ctypes.c_void_p)]
+                ("timing_events", ctypes.c_void_p), ("q_mean", ctypes.c_int32)]
 
 
 class CalibReport(ctypes.Structure):
@@ -155,10 +155,10 @@ def shape_of(q, k, cu_seqlens=None, max_seqlen=None) -> Shape:
     return Shape(cu_seqlens.numel() - 1, hq, k.shape[1], d, int(max_seqlen), t, cu_seqlens)
 
 
-def hifa4_workspace_bytes(shape: Shape, operands: int = OPERANDS_HIF4) -> int:
+def hifa4_workspace_bytes(shape: Shape, operands: int = OPERANDS_HIF4, q_mean: bool = False) -> int:
     lib = load_library()
     p = shape.problem()
-    o = FwdOptions(NORM_PREORDER, operands, 0, None, None, None)
+    o = FwdOptions(NORM_PREORDER, operands, 0, None, None, None, 1 if q_mean else 0)
     return int(lib.hifa4_workspace_bytes(ctypes.byref(p), ctypes.byref(o)))
 
 
@@ -240,11 +240,13 @@ _default_ws = Workspace()
 
 def hifa4_attention_fwd(q, k, v, s=None, cu_seqlens=None, max_seqlen=None, norm: int = NORM_PREORDER,
                         operands: int = OPERANDS_HIF4, smooth_qk: Optional[bool] = None, debug_p: bool = False,
-                        out=None, lse=None, workspace: Optional[Workspace] = None, timing_events=None):
+                        out=None, lse=None, workspace: Optional[Workspace] = None, timing_events=None,
+                        q_mean: bool = False):
     """HiFA4 causal prefill forward.  Returns (o, lse) or, with debug_p,
     (o, lse, p_codes uint8 [Hq,T,NB,32], p_meta int32 [Hq,T,NB]).
     timing_events: optional three recorded torch.cuda.Event objects (before
-    the pre-pass, before the attention kernel, after it)."""
+    the pre-pass, before the attention kernel, after it).  q_mean: the Q-Mean
+    auxiliary (HIF4 operands only)."""
     torch = _torch()
     for t, n in ((q, "q"), (k, "k"), (v, "v")):
         _require(t, torch.float16, n)
@@ -265,7 +267,7 @@ def hifa4_attention_fwd(q, k, v, s=None, cu_seqlens=None, max_seqlen=None, norm:
     if timing_events is not None:
         ev_arr = (ctypes.c_void_p * 3)(*[e.cuda_event for e in timing_events])
     opt = FwdOptions(norm, operands, 1 if smooth_qk else 0, _ptr(pc), _ptr(pm),
-                     ctypes.cast(ev_arr, ctypes.c_void_p) if ev_arr is not None else None)
+                     ctypes.cast(ev_arr, ctypes.c_void_p) if ev_arr is not None else None, 1 if q_mean else 0)
     p = sh.problem()
     need = int(lib.hifa4_workspace_bytes(ctypes.byref(p), ctypes.byref(opt)))
     ws = (workspace or _default_ws).get(need, dev)

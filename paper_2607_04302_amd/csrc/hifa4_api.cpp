@@ -68,7 +68,9 @@ size_t hifa4_workspace_bytes(const hifa4_problem* p, const hifa4_fwd_options* op
   Dims d;
   if (check_problem(p, &d) != HIFA4_OK) return 0;
   const bool fp16 = opt && opt->operands == HIFA4_OPERANDS_FP16;
-  const size_t chunk = fp16 ? hifa4::chunk_layout_fp16(p->head_dim).bytes : hifa4::chunk_layout_hif4(p->head_dim / 64).bytes;
+  const bool qmean = opt && opt->q_mean != 0;
+  const size_t chunk = fp16 ? hifa4::chunk_layout_fp16(p->head_dim).bytes
+                            : hifa4::chunk_layout_hif4(p->head_dim / 64, qmean).bytes;
   return chunk * (size_t)p->batch * p->num_heads_kv * std::max(1, d.NB);
 }
 
@@ -121,6 +123,9 @@ hifa4_status hifa4_attention_fwd(const hifa4_problem* p, const hifa4_fwd_options
   if ((opt->debug_p_codes == nullptr) != (opt->debug_p_meta == nullptr))
     return fail(HIFA4_ERR_INVALID_ARGUMENT, "debug_p_codes and debug_p_meta must both be set or both be NULL");
   const bool fp16 = opt->operands == HIFA4_OPERANDS_FP16;
+  if (fp16 && opt->q_mean)
+    return fail(HIFA4_ERR_UNSUPPORTED, "q_mean applies to HIF4 operands only");
+  const bool qmean = opt->q_mean != 0;
   const float* sm = (!fp16 && opt->smooth_qk) ? s : nullptr;
   if (!fp16 && opt->smooth_qk && !s) return fail(HIFA4_ERR_INVALID_ARGUMENT, "smooth_qk set but s is NULL");
   if (d.tokens == 0 || d.S == 0) return HIFA4_OK;
@@ -132,7 +137,7 @@ hifa4_status hifa4_attention_fwd(const hifa4_problem* p, const hifa4_fwd_options
   hipError_t e = hipSuccess;
   if (ev && (e = hipEventRecord(ev[0], hs)) != hipSuccess) return hip_fail(e, "timing event");
   e = hifa4::launch_prep_kv((const hifa4::half_t*)k, (const hifa4::half_t*)v, sm, p->cu_seqlens, (uint8_t*)workspace,
-                            p->batch, d.S, d.NB, p->num_heads_kv, p->head_dim, fp16, hs);
+                            p->batch, d.S, d.NB, p->num_heads_kv, p->head_dim, fp16, qmean, hs);
   if (e != hipSuccess) return hip_fail(e, "K/V pre-pass");
   if (ev && (e = hipEventRecord(ev[1], hs)) != hipSuccess) return hip_fail(e, "timing event");
   hifa4::AttnArgs a;
@@ -152,7 +157,7 @@ hifa4_status hifa4_attention_fwd(const hifa4_problem* p, const hifa4_fwd_options
   a.D = p->head_dim;
   a.total_tokens = (int)d.tokens;
   a.c = (float)(1.4426950408889634 / std::sqrt((double)p->head_dim));
-  e = hifa4::launch_attention(a, opt->norm, fp16, hs);
+  e = hifa4::launch_attention(a, opt->norm, fp16, qmean, hs);
   if (e != hipSuccess) return hip_fail(e, "attention kernel");
   if (ev && (e = hipEventRecord(ev[2], hs)) != hipSuccess) return hip_fail(e, "timing event");
   return HIFA4_OK;

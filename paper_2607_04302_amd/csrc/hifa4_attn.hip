@@ -402,8 +402,8 @@ __device__ __forceinline__ void load_q_half_group(const half_t* __restrict__ src
   }
 }
 
-__device__ __forceinline__ void quantize_q_half_group(const QRaw& r, bool smooth, float c, i8_t& qop, float& wq) {
-  h2_t x[16];
+// Smooth-QK of the raw half-group: fp16(q*s) per element (or q unchanged).
+__device__ __forceinline__ void smooth_half_group(const QRaw& r, bool smooth, h2_t x[16]) {
 #pragma unroll
   for (int i = 0; i < 16; ++i) x[i] = r.x[i];
   if (smooth) {
@@ -413,6 +413,47 @@ __device__ __forceinline__ void quantize_q_half_group(const QRaw& r, bool smooth
       x[2 * v + 1] = smooth_mul2(x[2 * v + 1], r.s[v].z, r.s[v].w);
     }
   }
+}
+
+// fp16 nearest to a float64 value (ties to even), rounded once: the value is
+// first rounded to odd in fp32 (which keeps 13 more significand bits than
+// fp16, enough for the second rounding to be exact), then to fp16.
+__device__ __forceinline__ half_t rn16_from_f64(double x) {
+  const float f = (float)x;
+  uint32_t b = __float_as_uint(f);
+  const double fd = (double)f;
+  if (fd != x) {
+    if (fabs(fd) > fabs(x)) b -= 1u;      // one fp32 step toward zero
+    b |= 1u;                             // sticky bit: round to odd
+  }
+  return (half_t)__uint_as_float(b);
+}
+
+// Q-Mean (Algorithm 1, the mean step): mu = fp16(sum of the row's D smoothed
+// values / D), the sum exact in float64, then Q_z = fp16(q~ - mu) in place
+// (one packed fp16 subtraction per pair, each difference rounded once).
+// The lane pair (l, l^32) holds the row; returns fp32(mu * c).
+template <int G>
+__device__ __forceinline__ float centre_q_row(h2_t (&x)[G][16], float c) {
+  double part = 0.0;
+#pragma unroll
+  for (int g = 0; g < G; ++g)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) part += (double)(float)x[g][i][0] + (double)(float)x[g][i][1];
+  part += __shfl_xor(part, 32);
+  const half_t mu = rn16_from_f64(part * (1.0 / (64.0 * G)));
+  const h2_t mu2 = {mu, mu};
+#pragma unroll
+  for (int g = 0; g < G; ++g)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) x[g][i] = x[g][i] - mu2;
+  return (float)mu * c;
+}
+
+__device__ __forceinline__ void quantize_q_half_group(const h2_t (&xin)[16], float c, i8_t& qop, float& wq) {
+  h2_t x[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) x[i] = xin[i];
   h2_t ax[16];
 #pragma unroll
   for (int i = 0; i < 16; ++i) ax[i] = habs2(x[i]);
@@ -464,13 +505,13 @@ struct Hif4State {
   float inv_rho;    // 1 / rho
 };
 
-template <int G, int NORM, bool DEBUG, bool MASK>
+template <int G, int NORM, bool DEBUG, bool QMEAN, bool MASK>
 __device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm, const uint8_t* cur, int J, int lane,
                                            int h, int col, int qi, bool row_ok, const i8_t (&qop)[G],
-                                           const float (&wq)[G], const i8_t& ones, Hif4State<G>& st,
+                                           const float (&wq)[G], float cmu, const i8_t& ones, Hif4State<G>& st,
                                            const ChunkStream& cs) {
   constexpr int DT = 2 * G;
-  constexpr ChunkLayout lay = chunk_layout_hif4(G);
+  constexpr ChunkLayout lay = chunk_layout_hif4(G, QMEAN);
   constexpr int CB = (int)lay.bytes;
   // ---- scores: S2 = fp16(acc), acc = fp32(d_0 w_0) then fused d_g w_g + acc,
   // with w_g = fp32(b_q,g/4 * c) (the softmax scale folded into the group scale).
@@ -493,11 +534,29 @@ __device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm,
                              acc[g], ks[g]);
     stream_piece<CB>(cs, 2 + t);
     float sacc[16];
+    if (QMEAN) {
+      // the accumulator starts from the Q-Mean correction fp32(fp32(mu c) kappa_j)
+      // of the lane's keys 32t + 8j + 4h + [0, 4), four keys at a time so that
+      // the corrections occupy no more registers than the dying accumulators
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      sacc[v] = acc[0][v] * wq[0];
+      for (int j = 0; j < 4; ++j) {
+        const float4 kp = *reinterpret_cast<const float4*>(cur + lay.kappa + 4 * (32 * t + 8 * j + 4 * h));
+        const float kv[4] = {kp.x, kp.y, kp.z, kp.w};
 #pragma unroll
-      for (int g = 1; g < G; ++g) sacc[v] = __builtin_fmaf(acc[g][v], wq[g], sacc[v]);
+        for (int i = 0; i < 4; ++i) {
+          float x = cmu * kv[i];
+#pragma unroll
+          for (int g = 0; g < G; ++g) x = __builtin_fmaf(acc[g][4 * j + i], wq[g], x);
+          sacc[4 * j + i] = x;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        sacc[v] = acc[0][v] * wq[0];
+#pragma unroll
+        for (int g = 1; g < G; ++g) sacc[v] = __builtin_fmaf(acc[g][v], wq[g], sacc[v]);
+      }
     }
 #pragma unroll
     for (int v2 = 0; v2 < 8; ++v2) s2[t][v2] = pack2_f16(sacc[2 * v2], sacc[2 * v2 + 1]);
@@ -678,12 +737,12 @@ __device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm,
   }
 }
 
-template <int G, int NORM, bool DEBUG>
+template <int G, int NORM, bool DEBUG, bool QMEAN>
 __global__ void __launch_bounds__(256, (G == 1 ? 4 : (G == 2 ? 3 : 1))) k_attn_hif4(AttnArgs a, int heads_per_wg, int qsub,
                                                                       int n_qtiles) {
   constexpr int D = 64 * G;
   constexpr int DT = D / 32;
-  constexpr ChunkLayout lay = chunk_layout_hif4(G);
+  constexpr ChunkLayout lay = chunk_layout_hif4(G, QMEAN);
   constexpr int cbytes = (int)lay.bytes;
   extern __shared__ __align__(16) uint8_t smem[];
   const TileMap tm = map_tile(a, heads_per_wg, qsub, n_qtiles);
@@ -706,10 +765,15 @@ __global__ void __launch_bounds__(256, (G == 1 ? 4 : (G == 2 ? 3 : 1))) k_attn_h
     load_q_half_group(src, sp, row_ok, raw[g]);
   }
   stage_chunk_async<cbytes>(smem, ws_base);
+  h2_t xs[G][16];
+#pragma unroll
+  for (int g = 0; g < G; ++g) smooth_half_group(raw[g], a.s != nullptr, xs[g]);
+  float cmu = 0.0f;
+  if (QMEAN) cmu = centre_q_row<G>(xs, a.c);
   i8_t qop[G];
   float wq[G];
 #pragma unroll
-  for (int g = 0; g < G; ++g) quantize_q_half_group(raw[g], a.s != nullptr, a.c, qop[g], wq[g]);
+  for (int g = 0; g < G; ++g) quantize_q_half_group(xs[g], a.c, qop[g], wq[g]);
 
   i8_t ones;
   {
@@ -745,9 +809,9 @@ __global__ void __launch_bounds__(256, (G == 1 ? 4 : (G == 2 ? 3 : 1))) k_attn_h
     const ChunkStream cs{smem + ((J + 1) & 1) * cbytes, ws_base + (size_t)(J + 1 < tm.nJ ? J + 1 : J) * cbytes,
                          wave_u};
     if (J < jw_last)
-      hif4_block<G, NORM, DEBUG, false>(a, tm, cur, J, lane, h, col, qi, row_ok, qop, wq, ones, st, cs);
+      hif4_block<G, NORM, DEBUG, QMEAN, false>(a, tm, cur, J, lane, h, col, qi, row_ok, qop, wq, cmu, ones, st, cs);
     else if (J == jw_last)
-      hif4_block<G, NORM, DEBUG, true>(a, tm, cur, J, lane, h, col, qi, row_ok, qop, wq, ones, st, cs);
+      hif4_block<G, NORM, DEBUG, QMEAN, true>(a, tm, cur, J, lane, h, col, qi, row_ok, qop, wq, cmu, ones, st, cs);
     else
       stream_pieces_from<cbytes>(cs, 0);
     wait_async_copies();
@@ -925,7 +989,7 @@ static hipError_t launch_k(K kern, const AttnArgs& a, size_t lds, hipStream_t st
   return hipGetLastError();
 }
 
-hipError_t launch_attention(const AttnArgs& a, int norm, bool fp16, hipStream_t st) {
+hipError_t launch_attention(const AttnArgs& a, int norm, bool fp16, bool qmean, hipStream_t st) {
   if (fp16) {
     const size_t lds = 2 * chunk_layout_fp16(a.D).bytes;
     switch (a.D) {
@@ -935,13 +999,18 @@ hipError_t launch_attention(const AttnArgs& a, int norm, bool fp16, hipStream_t 
     }
     return hipErrorInvalidValue;
   }
-  const size_t lds = 2 * chunk_layout_hif4(a.D / 64).bytes;
+  const size_t lds = 2 * chunk_layout_hif4(a.D / 64, qmean).bytes;
   const bool dbg = a.dbg_codes != nullptr;
-#define HIFA4_DISPATCH(G)                                                                            \
-  do {                                                                                               \
-    if (norm == 0)                                                                                   \
-      return dbg ? launch_k(k_attn_hif4<G, 0, true>, a, lds, st) : launch_k(k_attn_hif4<G, 0, false>, a, lds, st); \
-    return dbg ? launch_k(k_attn_hif4<G, 1, true>, a, lds, st) : launch_k(k_attn_hif4<G, 1, false>, a, lds, st);   \
+#define HIFA4_DISPATCH_Q(G, QM)                                                                          \
+  do {                                                                                                   \
+    if (norm == 0)                                                                                       \
+      return dbg ? launch_k(k_attn_hif4<G, 0, true, QM>, a, lds, st) : launch_k(k_attn_hif4<G, 0, false, QM>, a, lds, st); \
+    return dbg ? launch_k(k_attn_hif4<G, 1, true, QM>, a, lds, st) : launch_k(k_attn_hif4<G, 1, false, QM>, a, lds, st);   \
+  } while (0)
+#define HIFA4_DISPATCH(G)              \
+  do {                                 \
+    if (qmean) HIFA4_DISPATCH_Q(G, true); \
+    HIFA4_DISPATCH_Q(G, false);        \
   } while (0)
   switch (a.D) {
     case 64: HIFA4_DISPATCH(1);
@@ -949,6 +1018,7 @@ hipError_t launch_attention(const AttnArgs& a, int norm, bool fp16, hipStream_t 
     case 256: HIFA4_DISPATCH(4);
   }
 #undef HIFA4_DISPATCH
+#undef HIFA4_DISPATCH_Q
   return hipErrorInvalidValue;
 }
 

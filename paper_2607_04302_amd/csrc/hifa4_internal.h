@@ -16,7 +16,7 @@ typedef _Float16 half_t;
 constexpr size_t kOpRecord = 64 * 24;
 
 struct ChunkLayout {
-  size_t k_op, k_scale, v_op, v_scale, bytes;
+  size_t k_op, k_scale, v_op, v_scale, kappa, bytes;
 };
 
 __host__ __device__ constexpr size_t round_up256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -25,16 +25,20 @@ __host__ __device__ constexpr size_t round_up256(size_t x) { return (x + 255) & 
 // (operand A = codes, B = zero, codes or negated codes; byte 0 / 1 of the
 // scale word are their E8M0 scales):
 //   K [2 halves][G][2 operands] records, K scale words [2][G][32 keys],
-//   V [D/32][2 operands] records, V scale words [D].
-__host__ __device__ constexpr ChunkLayout chunk_layout_hif4(int G) {
+//   V [D/32][2 operands] records, V scale words [D],
+//   with Q-Mean: kappa [64 keys] fp32, the exact channel sum of each smoothed
+//   key rounded once.
+__host__ __device__ constexpr ChunkLayout chunk_layout_hif4(int G, bool qmean = false) {
   ChunkLayout c{};
   c.k_op = 0;
   c.k_scale = round_up256((size_t)2 * G * 2 * kOpRecord);
   c.v_op = c.k_scale + round_up256((size_t)2 * G * 32 * 4);
   c.v_scale = c.v_op + round_up256((size_t)(2 * G) * 2 * kOpRecord);
+  c.kappa = c.v_scale + round_up256((size_t)64 * G * 4);
+  const size_t end = c.kappa + (qmean ? round_up256((size_t)64 * 4) : 0);
   // a multiple of 1 KiB: the attention kernel streams chunks into LDS in
   // whole-wave pieces of 64 lanes x 16 bytes
-  c.bytes = (c.v_scale + round_up256((size_t)64 * G * 4) + 1023) & ~(size_t)1023;
+  c.bytes = (end + 1023) & ~(size_t)1023;
   return c;
 }
 
@@ -67,10 +71,10 @@ hipError_t launch_quant_rows(const half_t* x, const float* s, uint8_t* codes, ui
 hipError_t launch_quant_v(const half_t* v, const int* cu, uint8_t* codes, uint32_t* meta, int batch, int S, int NB,
                           int heads_kv, int D, hipStream_t st);
 hipError_t launch_prep_kv(const half_t* k, const half_t* v, const float* s, const int* cu, uint8_t* ws, int batch,
-                          int S, int NB, int heads_kv, int D, bool fp16, hipStream_t st);
+                          int S, int NB, int heads_kv, int D, bool fp16, bool qmean, hipStream_t st);
 hipError_t launch_calib(const half_t* q, const half_t* k, int n, int S, int hq, int hkv, int D, uint32_t* stats,
                         unsigned long long* hist, hipStream_t st);
 hipError_t launch_selftest_exp2(const half_t* x, half_t* y, long n, hipStream_t st);
-hipError_t launch_attention(const AttnArgs& a, int norm, bool fp16, hipStream_t st);
+hipError_t launch_attention(const AttnArgs& a, int norm, bool fp16, bool qmean, hipStream_t st);
 
 }  // namespace hifa4

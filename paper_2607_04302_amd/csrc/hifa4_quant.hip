@@ -216,7 +216,8 @@ __device__ __forceinline__ void store_split_operand(uint8_t* rec, int lane, cons
 
 __global__ void __launch_bounds__(512) k_prep_kv_hif4(const half_t* __restrict__ k, const half_t* __restrict__ v,
                                                       const float* __restrict__ s, const int* __restrict__ cu,
-                                                      uint8_t* __restrict__ ws, int S, int NB, int heads_kv, int G) {
+                                                      uint8_t* __restrict__ ws, int S, int NB, int heads_kv, int G,
+                                                      bool qmean) {
   // workgroup (J, hk, 2b + role): role 0 quantizes K, role 1 V, of block J
   extern __shared__ __align__(16) uint8_t sm[];
   const int J = blockIdx.x, hk = blockIdx.y, b = blockIdx.z >> 1;
@@ -225,7 +226,7 @@ __global__ void __launch_bounds__(512) k_prep_kv_hif4(const half_t* __restrict__
   const int t0 = seq_start(cu, b, S);
   const int L = seq_len(cu, b, S);
   if (64 * J >= L) return;
-  const ChunkLayout lay = chunk_layout_hif4(G);
+  const ChunkLayout lay = chunk_layout_hif4(G, qmean);
   uint8_t* chunk = ws + ((size_t)(b * heads_kv + hk) * NB + J) * lay.bytes;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, h = lane >> 5;
   float x[32], o[32];
@@ -251,6 +252,23 @@ __global__ void __launch_bounds__(512) k_prep_kv_hif4(const half_t* __restrict__
     } else {
 #pragma unroll
       for (int c = 0; c < 32; ++c) x[c] = 0.0f;
+    }
+    if (qmean) {
+      // Q-Mean key sums (Algorithm 1's correction term): the exact sum of the
+      // key's smoothed channels in float64 (any 256 fp16 values sum exactly),
+      // one partial per (32-key half, group) in LDS, then rounded once to fp32.
+      double part = 0.0;
+#pragma unroll
+      for (int c = 0; c < 32; ++c) part += (double)x[c];
+      part += __shfl_xor(part, 32);
+      double* parts = reinterpret_cast<double*>(sm + 2 * D * sizeof(float));     // [2][G][32]
+      if (h == 0) parts[(t * G + g) * 32 + (lane & 31)] = part;
+      __syncthreads();
+      if (g == 0 && h == 0) {
+        double sum = 0.0;
+        for (int gg = 0; gg < G; ++gg) sum += parts[(t * G + gg) * 32 + (lane & 31)];
+        reinterpret_cast<float*>(chunk + lay.kappa)[32 * t + (lane & 31)] = (float)sum;
+      }
     }
     const GroupMeta gm = quantize_split<kRows>(x, o, h);
     h32_t hv;
@@ -426,13 +444,13 @@ hipError_t launch_quant_v(const half_t* v, const int* cu, uint8_t* codes, uint32
 }
 
 hipError_t launch_prep_kv(const half_t* k, const half_t* v, const float* s, const int* cu, uint8_t* ws, int batch,
-                          int S, int NB, int heads_kv, int D, bool fp16, hipStream_t st) {
+                          int S, int NB, int heads_kv, int D, bool fp16, bool qmean, hipStream_t st) {
   dim3 grid(NB, heads_kv, batch);
   if (fp16)
     k_prep_kv_fp16<<<grid, dim3(256), 0, st>>>(k, v, cu, ws, S, NB, heads_kv, D);
   else
     k_prep_kv_hif4<<<dim3(NB, heads_kv, 2 * batch), dim3(64 * 2 * (D / 64)), 64 * D * sizeof(half_t), st>>>(
-        k, v, s, cu, ws, S, NB, heads_kv, D / 64);
+        k, v, s, cu, ws, S, NB, heads_kv, D / 64, qmean);
   return hipGetLastError();
 }
 

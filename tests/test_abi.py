@@ -55,6 +55,8 @@ def test_validation_codes(lib):
     assert _fwd(lib, _p(), opt=h.FwdOptions(7, 0, 0, None, None, None)) == -1
     assert _fwd(lib, _p(), opt=h.FwdOptions(0, 0, 1, None, None, None)) == -1      # smooth without s
     assert _fwd(lib, _p(), opt=h.FwdOptions(0, 0, 0, 1, None, None)) == -1         # half a debug dump
+    assert _fwd(lib, _p(), opt=h.FwdOptions(0, 1, 0, None, None, None, 1)) == -2   # Q-Mean with fp16 operands
+    assert "q_mean" in h.hifa4_last_error()
     assert _fwd(lib, _p(), ws=16) == -3
     assert "workspace" in h.hifa4_last_error()
     assert lib.hifa4_selftest_exp2(None, None, -1, None) == -1
@@ -64,9 +66,13 @@ def test_workspace_sizes(lib):
     p = _p(max_seqlen=4096, num_heads_q=32, num_heads_kv=8)
     o = h.FwdOptions(0, 0, 0, None, None, None)
     n = lib.hifa4_workspace_bytes(ctypes.byref(p), ctypes.byref(o))
-    # 64 blocks x 8 kv heads x (3 x 6 KB K operand variants + 512 B K scale
-    # words + 6 KB V operand + 512 B V scale words)
+    # 64 blocks x 8 kv heads x (K: 2 key halves x 2 groups x 2 operands of
+    # 1536 B + 512 B of scale words; V: 4 channel tiles x 2 operands of 1536 B
+    # + 512 B of scale words)
     assert n == 64 * 8 * 25600
+    # Q-Mean adds 256 B of key sums per chunk, rounded to a whole KiB
+    oq = h.FwdOptions(0, 0, 0, None, None, None, 1)
+    assert lib.hifa4_workspace_bytes(ctypes.byref(p), ctypes.byref(oq)) == 64 * 8 * 26624
     o16 = h.FwdOptions(0, 1, 0, None, None, None)
     assert lib.hifa4_workspace_bytes(ctypes.byref(p), ctypes.byref(o16)) == 64 * 8 * 32768
     assert lib.hifa4_workspace_bytes(ctypes.byref(_p(head_dim=80)), ctypes.byref(o)) == 0

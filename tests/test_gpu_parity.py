@@ -86,7 +86,7 @@ def test_quantize_v_bitexact(h):
 
 
 def _run_and_compare(h, q, k, v, cu, s, max_seqlen, norm="preorder", heads=None, rows=None, check_p=True,
-                     seqs=None):
+                     seqs=None, q_mean=False):
     """Runs the HIP forward on the whole problem, the oracle on the sampled
     (sequence, head, row) set, and compares O, LSE and (check_p) the P^ dump.
     Only the sampled slices of the GPU outputs are copied to the host."""
@@ -94,10 +94,10 @@ def _run_and_compare(h, q, k, v, cu, s, max_seqlen, norm="preorder", heads=None,
     cu_t = None if cu is None else to_gpu(cu)
     nm = h.NORM_PREORDER if norm == "preorder" else h.NORM_INCONSISTENT
     res = h.hifa4_attention_fwd(to_gpu(q), to_gpu(k), to_gpu(v), None if s is None else to_gpu(s),
-                                cu_seqlens=cu_t, max_seqlen=max_seqlen, norm=nm, debug_p=check_p)
+                                cu_seqlens=cu_t, max_seqlen=max_seqlen, norm=nm, debug_p=check_p, q_mean=q_mean)
     o, lse = res[0], res[1]
     ref = oatt.attention_fwd(q, k, v, s, cu_seqlens=cu, norm=norm, heads=heads, rows=rows, want_p=check_p,
-                             seqs=seqs)
+                             seqs=seqs, q_mean=q_mean)
     if cu is None:
         bsz, S = q.shape[:2]
         cuv = np.arange(bsz + 1) * S
@@ -255,3 +255,43 @@ def test_wide_d256_sampled(h):
     _say("wide_d256 inconsistent")
     _run_and_compare(h, q, k, v, None, s, w.seqlen, norm="inconsistent", heads=[6], rows=rows, seqs=[1],
                      check_p=False)
+
+
+# ---------------------------------------------------------------------------
+# Q-Mean auxiliary (Algorithm 1, the mean step and the score correction).
+# mu, Q_z and the key sums kappa enter every score, so bit-exact P^ codes on
+# every row check all three against the oracle's definitions.
+
+def test_qmean_tiny_full_parity(h):
+    w = WORKLOADS["tiny_s256"]
+    q, k, v, _ = make_inputs(w)
+    qc, kc = make_calibration(w)
+    s, _ = osmooth.calibrate(qc, kc, w.heads_kv, w.alpha)
+    _say("tiny_s256 q_mean")
+    _run_and_compare(h, q, k, v, None, s, w.seqlen, q_mean=True)
+
+
+@pytest.mark.parametrize("d,hq,hkv,lens,seed,bias", [
+    (128, 4, 1, (300, 65, 64, 1, 190), 1, 2.0),   # DC-biased queries, GQA x4, ragged tails
+    (64, 2, 2, (129, 511), 2, -1.5),               # D=64
+    (256, 4, 2, (200, 33), 3, 0.75),               # D=256
+    (128, 8, 8, (97,), 4, 0.0),                    # no bias: mu near zero
+])
+def test_qmean_varlen_parity(h, d, hq, hkv, lens, seed, bias):
+    q, k, v, cu = small_case(heads_q=hq, heads_kv=hkv, head_dim=d, seqlens=lens, seed=seed, q_bias=bias)
+    s = np.exp(np.random.default_rng(seed).uniform(-1, 1.5, (hkv, d))).astype(np.float32)
+    _say("q_mean varlen", d, hq, hkv, lens, bias)
+    _run_and_compare(h, q, k, v, cu, s, max(lens), q_mean=True)
+    _run_and_compare(h, q, k, v, cu, None, max(lens), norm="inconsistent", q_mean=True)
+
+
+def test_qmean_qwen3_shape_sampled(h):
+    """Q-Mean on the Qwen3-8B-shaped S=4096 workload, full size, sampled heads
+    and rows, P^ codes bit-exact."""
+    w = WORKLOADS["qwen3_8b_s4096"]
+    q, k, v, _ = make_inputs(w)
+    qc, kc = make_calibration(w, n=4)
+    s, _ = osmooth.calibrate(qc, kc, w.heads_kv, w.alpha)
+    rows = [0, 1, 63, 64, 2047, 4031, 4095]
+    _say("qwen3 sampled q_mean")
+    _run_and_compare(h, q, k, v, None, s, w.seqlen, heads=[0, 5, 31], rows=rows, q_mean=True)
