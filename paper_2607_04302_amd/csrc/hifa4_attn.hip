@@ -839,14 +839,17 @@ __global__ void __launch_bounds__(256, (G == 1 ? 4 : (G == 2 ? 3 : 1))) k_attn_h
 }
 
 // ---------------------------------------------------------------------------
-// FP16-operand variant (the C16V16 reference): same decomposition and softmax,
-// 32x32x16 f16 MFMAs, P in fp16 as the PV operand, O accumulated by the MFMA,
-// l = rowsum(P).
+// FP16-operand variant (the C16V16 reference): same decomposition, chunk
+// stream and softmax as the HiFA4 kernel, 32x32x16 f16 MFMAs, P in fp16 as the
+// PV operand, O accumulated by the MFMA, l = rowsum(P).  The two 32-key
+// halves of S^T and the D/32 channel tiles of O^T are independent MFMA
+// chains, issued interleaved.
 template <int D>
-__global__ void __launch_bounds__(256) k_attn_fp16(AttnArgs a, int heads_per_wg, int qsub, int n_qtiles) {
+__global__ void __launch_bounds__(256, (D <= 128 ? 2 : 1)) k_attn_fp16(AttnArgs a, int heads_per_wg, int qsub, int n_qtiles) {
   constexpr int KC = D / 16;
   constexpr int DT = D / 32;
   constexpr ChunkLayout lay = chunk_layout_fp16(D);
+  constexpr int cbytes = (int)lay.bytes;
   extern __shared__ __align__(16) uint8_t smem[];
   const TileMap tm = map_tile(a, heads_per_wg, qsub, n_qtiles);
   if (!tm.wg_live) return;
@@ -854,6 +857,8 @@ __global__ void __launch_bounds__(256) k_attn_fp16(AttnArgs a, int heads_per_wg,
   const int qi = tm.qw + col;
   const bool row_ok = tm.active && qi < tm.L;
   const int jw_last = tm.active ? (min(tm.qw + 31, tm.L - 1)) / 64 : -1;
+  const uint8_t* ws_base = a.ws + ((size_t)(tm.b * a.hkv + tm.hk) * a.NB) * lay.bytes;
+  const int wave_u = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
 
   h8_t qf[KC];
 #pragma unroll
@@ -863,6 +868,7 @@ __global__ void __launch_bounds__(256) k_attn_fp16(AttnArgs a, int heads_per_wg,
     else
       for (int e = 0; e < 8; ++e) qf[kc][e] = (half_t)0.0f;
   }
+  stage_chunk_async<cbytes>(smem, ws_base);
   f16v_t O[DT];
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt)
@@ -870,31 +876,30 @@ __global__ void __launch_bounds__(256) k_attn_fp16(AttnArgs a, int heads_per_wg,
     for (int v = 0; v < 16; ++v) O[dt][v] = 0.0f;
   half_t m_run = (half_t)(-__builtin_inff());
   float l_sum = 0.0f;
-
-  const uint8_t* ws_base = a.ws + ((size_t)(tm.b * a.hkv + tm.hk) * a.NB) * lay.bytes;
-  constexpr int cbytes = (int)lay.bytes;
-  stage_chunk(smem, ws_base, cbytes);
+  wait_async_copies();
   __syncthreads();
 
   for (int J = 0; J < tm.nJ; ++J) {
     set_priority_by_work_left(tm.nJ - J);
     const uint8_t* cur = smem + (J & 1) * cbytes;
-    const bool has_next = J + 1 < tm.nJ;
+    const ChunkStream cs{smem + ((J + 1) & 1) * cbytes, ws_base + (size_t)(J + 1 < tm.nJ ? J + 1 : J) * cbytes,
+                         wave_u};
     if (tm.active && J <= jw_last) {
+      stream_piece<cbytes>(cs, 0);
+      f16v_t acc[2] = {};
+#pragma unroll
+      for (int kc = 0; kc < KC; ++kc)
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          const h8_t kf = *reinterpret_cast<const h8_t*>(cur + lay.k_op + ((size_t)(t * KC + kc) * 64 + lane) * 16);
+          acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf, qf[kc], acc[t], 0, 0, 0);
+        }
+      stream_piece<cbytes>(cs, 1);
       h2_t s2[2][8];
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        f16v_t acc = {};
+      for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int kc = 0; kc < KC; ++kc) {
-          const h8_t kf = *reinterpret_cast<const h8_t*>(cur + lay.k_op + ((size_t)(t * KC + kc) * 64 + lane) * 16);
-          acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf, qf[kc], acc, 0, 0, 0);
-        }
-#pragma unroll
-        for (int v2 = 0; v2 < 8; ++v2) {
-          s2[t][v2] = scale2_to_f16(acc[2 * v2], acc[2 * v2 + 1], a.c);
-        }
-      }
+        for (int v2 = 0; v2 < 8; ++v2) s2[t][v2] = scale2_to_f16(acc[t][2 * v2], acc[t][2 * v2 + 1], a.c);
       if (64 * J + 63 > tm.qw) {
         const half_t ninf = (half_t)(-__builtin_inff());
 #pragma unroll
@@ -903,29 +908,32 @@ __global__ void __launch_bounds__(256) k_attn_fp16(AttnArgs a, int heads_per_wg,
           for (int v = 0; v < 16; ++v)
             if (64 * J + key_of(t, h, v) > qi) s2[t][v >> 1][v & 1] = ninf;
       }
-      h2_t mx2 = s2[0][0];
+      h2_t mx2 = hmax16(&s2[0][0]);
+      mx2 = hmax_halves(max_with_partner(mx2));
+      const h2_t mr2 = {m_run, m_run};
+      const h2_t mn2 = hmax2(mr2, mx2);
+      stream_piece<cbytes>(cs, 2);
+      h2_t p2[2][8];
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int v2 = 0; v2 < 8; ++v2) mx2 = __builtin_elementwise_max(mx2, s2[t][v2]);
-      half_t mx = hmax(mx2[0], mx2[1]);
-      mx = hmax(mx, (half_t)shfl_xor32((float)mx));
-      const half_t m_new = hmax(m_run, mx);
-      const h2_t mn2 = {m_new, m_new};
-      h2_t p2[2][8];
+        for (int q = 0; q < 2; ++q) {
+          h2_t xin[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) xin[i] = s2[t][4 * q + i] - mn2;
+          exp2_h2x4(xin, &p2[t][4 * q]);
+        }
       float ps = 0.0f;
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int v2 = 0; v2 < 8; ++v2) {
-          p2[t][v2] = exp2_h2(s2[t][v2] - mn2);
-          ps += (float)p2[t][v2][0] + (float)p2[t][v2][1];
-        }
-      ps += shfl_xor32(ps);
-      const h2_t rr = exp2_h2(h2_t{(half_t)(m_run - m_new), (half_t)0});
+        for (int v2 = 0; v2 < 8; ++v2) ps = __builtin_amdgcn_fdot2(p2[t][v2], h2_t{(half_t)1, (half_t)1}, ps, false);
+      ps = add_with_partner(ps);
+      const h2_t rr = exp2_h2(h2_t{(half_t)(mr2[0] - mn2[0]), (half_t)0});
       const float r = (float)rr[0];
-      m_run = m_new;
+      m_run = mn2[0];
       l_sum = l_sum * r + ps;
+      stream_piece<cbytes>(cs, 3);
       if (__builtin_amdgcn_ballot_w64(r != 1.0f) != 0) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
@@ -945,14 +953,19 @@ __global__ void __launch_bounds__(256) k_attn_fp16(AttnArgs a, int heads_per_wg,
         }
       }
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
+      for (int c = 0; c < 4; ++c) {
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
+        for (int dt = 0; dt < DT; ++dt) {
           const h8_t vf = *reinterpret_cast<const h8_t*>(cur + lay.v_op + ((size_t)(dt * 4 + c) * 64 + lane) * 16);
           O[dt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pb[c], O[dt], 0, 0, 0);
         }
+        stream_piece<cbytes>(cs, 4 + c);
+      }
+      stream_pieces_from<cbytes>(cs, 8);
+    } else {
+      stream_pieces_from<cbytes>(cs, 0);
     }
-    if (has_next) stage_chunk(smem + ((J + 1) & 1) * cbytes, ws_base + (size_t)(J + 1) * cbytes, cbytes);
+    wait_async_copies();
     __syncthreads();
   }
   if (row_ok) {
