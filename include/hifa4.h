@@ -94,9 +94,14 @@ typedef enum {
 } hifa4_norm;
 
 typedef enum {
-  HIFA4_OPERANDS_HIF4 = 0,  /* both contractions on HIF4 operands (C4V16)     */
-  HIFA4_OPERANDS_FP16 = 1   /* same loop on fp16 operands, no quantization and
-                               no smoothing: the FP16 reference (C16V16) */
+  HIFA4_OPERANDS_HIF4 = 0,   /* both contractions on HIF4 operands (C4V16)     */
+  HIFA4_OPERANDS_FP16 = 1,   /* same loop on fp16 operands, no quantization and
+                                no smoothing: the FP16 reference (C16V16) */
+  HIFA4_OPERANDS_P_ONLY = 2  /* P-only local operator (the study the paper
+                                defers, Section 4.5): Q, K and V stay fp16
+                                (no smoothing), scores and softmax as in the
+                                FP16 reference, P^ = HIF4(P) feeds the PV
+                                product; the normalizer follows opt->norm */
 } hifa4_operands;
 
 /* Options of hifa4_attention_fwd.
@@ -109,7 +114,7 @@ typedef enum {
  *                  its sequence) sees, other entries are left untouched;
  *   debug_p_meta   NULL, or a DEVICE uint32 buffer [num_heads_q, T, NB] with
  *                  the matching metadata words.  Both or neither.
- * Debug dumps are only produced for HIFA4_OPERANDS_HIF4.
+ * Debug dumps are produced for HIFA4_OPERANDS_HIF4 and _P_ONLY.
  *   timing_events  NULL, or a HOST array of three hipEvent_t (created by the
  *                  caller) that the call records on `stream` before the K/V
  *                  pre-pass, between the pre-pass and the attention kernel,

@@ -188,6 +188,8 @@ def attention_fwd(q, k, v, s=None, cu_seqlens=None, norm="preorder", operands="h
     [Hkv, D] or None (no smoothing).  ``heads``/``seqs``/``rows`` restrict the
     computation to a sample (rows are positions within each sequence).
     ``q_mean`` adds the Q-Mean auxiliary (HIF4 operands only).
+    ``operands``: "hif4", "fp16" (no quantization, no smoothing) or "p_only"
+    (Q, K, V unquantized fp16, no smoothing; only P is HIF4-quantized).
     Returns a dict keyed by (seq, head) with o (float64 O/l), o16, lse, and,
     with want_p, the canonical P^ codes/metadata per (row, block)."""
     qv, kv, vv, cu = _as_varlen(q, k, v, cu_seqlens)
@@ -228,9 +230,11 @@ def attention_fwd(q, k, v, s=None, cu_seqlens=None, norm="preorder", operands="h
                 s2 = scores_hif4(unit_operands(qf).reshape(len(rr), d), qf["scale"], khat, d, corr)
                 res = online_softmax(s2, vcache[hk], rr, length, True, want_p=want_p)
             else:
+                # "fp16": the FP16-operand reference; "p_only": the same scores
+                # and V with P^ = HIF4(P) as the PV operand (P-only local operator)
                 s2 = scores_fp16(qs[rr], ks, d)
                 vop = np.zeros((-(-length // BLOCK) * BLOCK, d)); vop[:length] = vs
-                res = online_softmax(s2, vop, rr, length, False, want_p=want_p)
+                res = online_softmax(s2, vop, rr, length, operands == "p_only", want_p=want_p)
             lsum = res["l_mis"] if norm == "inconsistent" else res["l_con"]
             o = res["o_num"] / lsum[:, None]
             res["o"] = o

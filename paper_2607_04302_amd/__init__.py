@@ -22,7 +22,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libhifa4.so")
 
 NORM_PREORDER, NORM_INCONSISTENT = 0, 1
-OPERANDS_HIF4, OPERANDS_FP16 = 0, 1
+OPERANDS_HIF4, OPERANDS_FP16, OPERANDS_P_ONLY = 0, 1, 2
 STATUS = {0: "HIFA4_OK", -1: "HIFA4_ERR_INVALID_ARGUMENT", -2: "HIFA4_ERR_UNSUPPORTED",
           -3: "HIFA4_ERR_WORKSPACE", -4: "HIFA4_ERR_HIP"}
 

@@ -67,7 +67,7 @@ const char* hifa4_last_error(void) { return g_last_error.c_str(); }
 size_t hifa4_workspace_bytes(const hifa4_problem* p, const hifa4_fwd_options* opt) {
   Dims d;
   if (check_problem(p, &d) != HIFA4_OK) return 0;
-  const bool fp16 = opt && opt->operands == HIFA4_OPERANDS_FP16;
+  const bool fp16 = opt && (opt->operands == HIFA4_OPERANDS_FP16 || opt->operands == HIFA4_OPERANDS_P_ONLY);
   const bool qmean = opt && opt->q_mean != 0;
   const size_t chunk = fp16 ? hifa4::chunk_layout_fp16(p->head_dim).bytes
                             : hifa4::chunk_layout_hif4(p->head_dim / 64, qmean).bytes;
@@ -117,12 +117,14 @@ hifa4_status hifa4_attention_fwd(const hifa4_problem* p, const hifa4_fwd_options
   if (!opt) return fail(HIFA4_ERR_INVALID_ARGUMENT, "options is NULL");
   if (opt->norm != HIFA4_NORM_PREORDER && opt->norm != HIFA4_NORM_INCONSISTENT)
     return fail(HIFA4_ERR_INVALID_ARGUMENT, "unknown norm %d", opt->norm);
-  if (opt->operands != HIFA4_OPERANDS_HIF4 && opt->operands != HIFA4_OPERANDS_FP16)
+  if (opt->operands != HIFA4_OPERANDS_HIF4 && opt->operands != HIFA4_OPERANDS_FP16 &&
+      opt->operands != HIFA4_OPERANDS_P_ONLY)
     return fail(HIFA4_ERR_INVALID_ARGUMENT, "unknown operands %d", opt->operands);
   if (!q || !k || !v || !o || !lse) return fail(HIFA4_ERR_INVALID_ARGUMENT, "null tensor pointer");
   if ((opt->debug_p_codes == nullptr) != (opt->debug_p_meta == nullptr))
     return fail(HIFA4_ERR_INVALID_ARGUMENT, "debug_p_codes and debug_p_meta must both be set or both be NULL");
-  const bool fp16 = opt->operands == HIFA4_OPERANDS_FP16;
+  // FP16 and P-only keep Q, K and V in fp16 (fp16 chunk layout, no smoothing)
+  const bool fp16 = opt->operands != HIFA4_OPERANDS_HIF4;
   if (fp16 && opt->q_mean)
     return fail(HIFA4_ERR_UNSUPPORTED, "q_mean applies to HIF4 operands only");
   const bool qmean = opt->q_mean != 0;
@@ -147,8 +149,9 @@ hifa4_status hifa4_attention_fwd(const hifa4_problem* p, const hifa4_fwd_options
   a.ws = (const uint8_t*)workspace;
   a.o = (hifa4::half_t*)o;
   a.lse = lse;
-  a.dbg_codes = fp16 ? nullptr : (uint8_t*)opt->debug_p_codes;
-  a.dbg_meta = fp16 ? nullptr : (uint32_t*)opt->debug_p_meta;
+  const bool dump = opt->operands != HIFA4_OPERANDS_FP16;
+  a.dbg_codes = dump ? (uint8_t*)opt->debug_p_codes : nullptr;
+  a.dbg_meta = dump ? (uint32_t*)opt->debug_p_meta : nullptr;
   a.batch = p->batch;
   a.S = d.S;
   a.NB = d.NB;
@@ -157,7 +160,7 @@ hifa4_status hifa4_attention_fwd(const hifa4_problem* p, const hifa4_fwd_options
   a.D = p->head_dim;
   a.total_tokens = (int)d.tokens;
   a.c = (float)(1.4426950408889634 / std::sqrt((double)p->head_dim));
-  e = hifa4::launch_attention(a, opt->norm, fp16, qmean, hs);
+  e = hifa4::launch_attention(a, opt->norm, opt->operands, qmean, hs);
   if (e != hipSuccess) return hip_fail(e, "attention kernel");
   if (ev && (e = hipEventRecord(ev[2], hs)) != hipSuccess) return hip_fail(e, "timing event");
   return HIFA4_OK;

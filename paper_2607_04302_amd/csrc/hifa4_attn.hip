@@ -497,6 +497,98 @@ __device__ __forceinline__ void quantize_q_half_group(const h2_t (&xin)[16], flo
   wq = (0.25f * bval) * c;      // b/4 exact, one rounding with c
 }
 
+// P^ = HIF4(P) of one 64-key block held in the S^T accumulator layout (lane
+// half h holds keys 32t + 8j + 4h + [0,4) of 4-block (t, j) in the packed
+// registers p2[t][2j], p2[t][2j+1]; the 8-blocks pair with lane l^32).  A is
+// the block maximum (an fp16 value).  Returns the operand values
+// o = u * 2^-sh in the order of the packed registers (slot 16t + 2v2 + e =
+// half e of p2[t][v2]) and the E6M2 base.  With DEBUG, a non-null dcodes /
+// dmeta receive the lane's share of the canonical codes and the metadata
+// word.
+struct PQuant {
+  h32_t ov;
+  uint32_t base;
+  float bval;
+};
+
+template <bool DEBUG>
+__device__ __forceinline__ PQuant quantize_p_block(const h2_t (&p2)[2][8], float A, int lane, int h, uint8_t* dcodes,
+                                                   uint32_t* dmeta) {
+  PQuant out;
+  // Maxima are packed in pairs of 4-blocks: a4[t][jp] = (A4(t, 2jp), A4(t, 2jp+1)).
+  const uint32_t base = e6m2_ceil(A);
+  const float bval = e6m2_value(base);
+  const float R = hif4_rcp_step(base);
+  // fp16 floors of the half and quarter ranges: an fp16 value x satisfies
+  // x <= 0.875b iff x <= floor16(0.875b) (round-toward-zero conversion).
+  const h2_t thr = __builtin_bit_cast(h2_t, __builtin_amdgcn_cvt_pkrtz(0.875f * bval, 0.4375f * bval));
+  const h2_t th_h = {thr[0], thr[0]}, th_q = {thr[1], thr[1]};
+  const uint32_t k400 = 0x04000400u, k5e00 = 0x5E005E00u;
+  h2_t cst[2][2];       // rounding constants of 4-blocks (t, 2jp), (t, 2jp+1)
+  h2_t a4s[2][2], a4p[2][2];
+  uint32_t e2bits = 0, e3bits = 0;
+  const int paddr = 4 * (lane ^ 32);
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int jp = 0; jp < 2; ++jp) {
+      const h2_t m0 = hmax2(p2[t][4 * jp], p2[t][4 * jp + 1]);       // 4-block 2jp, two partial maxima
+      const h2_t m1 = hmax2(p2[t][4 * jp + 2], p2[t][4 * jp + 3]);   // 4-block 2jp+1
+      a4s[t][jp] = hmax_pairs(m0, m1);
+      a4p[t][jp] = __builtin_bit_cast(h2_t, partner_bperm(__builtin_bit_cast(uint32_t, a4s[t][jp]), paddr));
+    }
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int jp = 0; jp < 2; ++jp) {
+      const h2_t a4 = a4s[t][jp];
+      const h2_t a8 = hmax2(a4, a4p[t][jp]);
+      cst[t][jp] = grid_consts(a4, a8, th_h, th_q, k400, k5e00);
+      if (DEBUG) {
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const int j = 2 * jp + e;
+          const bool e2 = a8[e] <= th_h[e];
+          const bool e3 = a4[e] <= (e2 ? th_q[e] : th_h[e]);
+          e2bits |= (uint32_t)e2 << (4 * t + j);
+          e3bits |= (uint32_t)e3 << (8 * t + 2 * j + h);
+          const bool e3o = a4p[t][jp][e] <= (e2 ? th_q[e] : th_h[e]);
+          e3bits |= (uint32_t)e3o << (8 * t + 2 * j + (h ^ 1));
+        }
+      }
+    }
+  // o = u * 2^-sh: one fp16 fma rounds P*R onto the grid 2^-sh, a packed
+  // subtraction removes the offset (both exact).
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int v2 = 0; v2 < 8; ++v2) {
+      // 4-block j = v2/2 of tile t: its constant is half (j & 1) of cst[t][j >> 1]
+      const h2_t cp = cst[t][v2 >> 2];
+      const h2_t tt = ((v2 >> 1) & 1) ? grid_round2<1>(p2[t][v2], R, cp) : grid_round2<0>(p2[t][v2], R, cp);
+      out.ov[16 * t + 2 * v2] = tt[0];
+      out.ov[16 * t + 2 * v2 + 1] = tt[1];
+    }
+  if (DEBUG && dcodes) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int q4 = 8 * t + 2 * j + h;
+        const int sh = (int)((e2bits >> (4 * t + j)) & 1u) + (int)((e3bits >> q4) & 1u);
+        uint32_t nib[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) nib[i] = (uint32_t)((float)out.ov[16 * t + 4 * j + i] * (float)(1 << sh));
+        dcodes[16 * t + 4 * j + 2 * h] = (uint8_t)(nib[0] | (nib[1] << 4));
+        dcodes[16 * t + 4 * j + 2 * h + 1] = (uint8_t)(nib[2] | (nib[3] << 4));
+      }
+    if (h == 0) *dmeta = base | (e2bits << 8) | (e3bits << 16);
+  }
+  out.base = base;
+  out.bval = bval;
+  return out;
+}
+
 template <int G>
 struct Hif4State {
   f16v_t O[2 * G];
@@ -602,88 +694,21 @@ __device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm,
 
   stream_piece<CB>(cs, 5);
   // ---- P^ = HIF4(P) over the block's 64 keys (P-Reordering).
-  // The lane's 4-block (t, j) holds keys 32t + 8j + 4h + [0,4), i.e. the
-  // packed registers p2[t][2j] and p2[t][2j+1].  Maxima are packed in pairs
-  // of 4-blocks: a4[t][jp] = (A4(t, 2jp), A4(t, 2jp+1)).
-  const uint32_t base = e6m2_ceil(A);
-  const float bval = e6m2_value(base);
-  const float R = hif4_rcp_step(base);
-  // fp16 floors of the half and quarter ranges: an fp16 value x satisfies
-  // x <= 0.875b iff x <= floor16(0.875b) (round-toward-zero conversion).
-  const h2_t thr = __builtin_bit_cast(h2_t, __builtin_amdgcn_cvt_pkrtz(0.875f * bval, 0.4375f * bval));
-  const h2_t th_h = {thr[0], thr[0]}, th_q = {thr[1], thr[1]};
-  const uint32_t k400 = 0x04000400u, k5e00 = 0x5E005E00u;
-  h2_t cst[2][2];       // rounding constants of 4-blocks (t, 2jp), (t, 2jp+1)
-  h2_t a4s[2][2], a4p[2][2];
-  uint32_t e2bits = 0, e3bits = 0;
-  const int paddr = 4 * (lane ^ 32);
-#pragma unroll
-  for (int t = 0; t < 2; ++t)
-#pragma unroll
-    for (int jp = 0; jp < 2; ++jp) {
-      const h2_t m0 = hmax2(p2[t][4 * jp], p2[t][4 * jp + 1]);       // 4-block 2jp, two partial maxima
-      const h2_t m1 = hmax2(p2[t][4 * jp + 2], p2[t][4 * jp + 3]);   // 4-block 2jp+1
-      a4s[t][jp] = hmax_pairs(m0, m1);
-      a4p[t][jp] = __builtin_bit_cast(h2_t, partner_bperm(__builtin_bit_cast(uint32_t, a4s[t][jp]), paddr));
-    }
-#pragma unroll
-  for (int t = 0; t < 2; ++t)
-#pragma unroll
-    for (int jp = 0; jp < 2; ++jp) {
-      const h2_t a4 = a4s[t][jp];
-      const h2_t a8 = hmax2(a4, a4p[t][jp]);
-      cst[t][jp] = grid_consts(a4, a8, th_h, th_q, k400, k5e00);
-      if (DEBUG) {
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-          const int j = 2 * jp + e;
-          const bool e2 = a8[e] <= th_h[e];
-          const bool e3 = a4[e] <= (e2 ? th_q[e] : th_h[e]);
-          e2bits |= (uint32_t)e2 << (4 * t + j);
-          e3bits |= (uint32_t)e3 << (8 * t + 2 * j + h);
-          const bool e3o = a4p[t][jp][e] <= (e2 ? th_q[e] : th_h[e]);
-          e3bits |= (uint32_t)e3o << (8 * t + 2 * j + (h ^ 1));
-        }
-      }
-    }
-  // o = u * 2^-sh: one fp16 fma rounds P*R onto the grid 2^-sh, a packed
-  // subtraction removes the offset (both exact).  B-operand slot s holds
-  // tile s/16, register s%16, i.e. the packed registers in order.
-  h32_t ov;
-#pragma unroll
-  for (int t = 0; t < 2; ++t)
-#pragma unroll
-    for (int v2 = 0; v2 < 8; ++v2) {
-      // 4-block j = v2/2 of tile t: its constant is half (j & 1) of cst[t][j >> 1]
-      const h2_t cp = cst[t][v2 >> 2];
-      const h2_t tt = ((v2 >> 1) & 1) ? grid_round2<1>(p2[t][v2], R, cp) : grid_round2<0>(p2[t][v2], R, cp);
-      ov[16 * t + 2 * v2] = tt[0];
-      ov[16 * t + 2 * v2 + 1] = tt[1];
-    }
-  const i6_t pk = __builtin_amdgcn_cvt_scalef32_pk32_fp6_f16(ov, 1.0f);
+  uint8_t* dcodes = nullptr;
+  uint32_t* dmeta = nullptr;
+  if (DEBUG && row_ok) {
+    const size_t e = ((size_t)tm.hq * a.total_tokens + tm.t0 + qi) * a.NB + J;
+    dcodes = a.dbg_codes + e * 32;
+    dmeta = a.dbg_meta + e;
+  }
+  const PQuant pq = quantize_p_block<DEBUG>(p2, A, lane, h, dcodes, dmeta);
+  const float bval = pq.bval;
+  const i6_t pk = __builtin_amdgcn_cvt_scalef32_pk32_fp6_f16(pq.ov, 1.0f);
   i8_t pop;
 #pragma unroll
   for (int i = 0; i < 6; ++i) pop[i] = pk[i];
   pop[6] = 0;
   pop[7] = 0;
-
-  if (DEBUG && row_ok) {
-    uint8_t* dc = a.dbg_codes + (((size_t)tm.hq * a.total_tokens + tm.t0 + qi) * a.NB + J) * 32;
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int q4 = 8 * t + 2 * j + h;
-        const int sh = (int)((e2bits >> (4 * t + j)) & 1u) + (int)((e3bits >> q4) & 1u);
-        uint32_t nib[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) nib[i] = (uint32_t)((float)ov[16 * t + 4 * j + i] * (float)(1 << sh));
-        dc[16 * t + 4 * j + 2 * h] = (uint8_t)(nib[0] | (nib[1] << 4));
-        dc[16 * t + 4 * j + 2 * h + 1] = (uint8_t)(nib[2] | (nib[3] << 4));
-      }
-    if (h == 0)
-      a.dbg_meta[((size_t)tm.hq * a.total_tokens + tm.t0 + qi) * a.NB + J] = base | (e2bits << 8) | (e3bits << 16);
-  }
 
   stream_piece<CB>(cs, 6);
   // ---- deferred rescale bookkeeping (lane-uniform factors).
@@ -986,6 +1011,193 @@ __global__ void __launch_bounds__(256, (D <= 128 ? 2 : 1)) k_attn_fp16(AttnArgs 
 }
 
 // ---------------------------------------------------------------------------
+// P-only local operator (the paper's deferred P-only study, Section 4.5 and
+// its limitations): Q, K and V stay fp16 and only P is quantized.  Scores and
+// the FP16 softmax are those of the FP16-operand kernel; P^ = HIF4(P) as in
+// the HiFA4 kernel; the PV product runs on the exact fp16 operand values
+// o = u * 2^-sh and an fp32 epilogue applies b_P/4 with the deferred rescale;
+// the normalizer accumulates the same P^ (NORM 0) or the pre-quantization P
+// (NORM 1).
+template <int D, int NORM, bool DEBUG>
+__global__ void __launch_bounds__(256, (D <= 128 ? 2 : 1)) k_attn_ponly(AttnArgs a, int heads_per_wg, int qsub,
+                                                                       int n_qtiles) {
+  constexpr int KC = D / 16;
+  constexpr int DT = D / 32;
+  constexpr ChunkLayout lay = chunk_layout_fp16(D);
+  constexpr int cbytes = (int)lay.bytes;
+  extern __shared__ __align__(16) uint8_t smem[];
+  const TileMap tm = map_tile(a, heads_per_wg, qsub, n_qtiles);
+  if (!tm.wg_live) return;
+  const int lane = threadIdx.x & 63, h = lane >> 5, col = lane & 31;
+  const int qi = tm.qw + col;
+  const bool row_ok = tm.active && qi < tm.L;
+  const int jw_last = tm.active ? (min(tm.qw + 31, tm.L - 1)) / 64 : -1;
+  const uint8_t* ws_base = a.ws + ((size_t)(tm.b * a.hkv + tm.hk) * a.NB) * lay.bytes;
+  const int wave_u = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+
+  h8_t qf[KC];
+#pragma unroll
+  for (int kc = 0; kc < KC; ++kc) {
+    if (row_ok)
+      qf[kc] = *reinterpret_cast<const h8_t*>(a.q + ((size_t)(tm.t0 + qi) * a.hq + tm.hq) * D + 16 * kc + 8 * h);
+    else
+      for (int e = 0; e < 8; ++e) qf[kc][e] = (half_t)0.0f;
+  }
+  stage_chunk_async<cbytes>(smem, ws_base);
+  f16v_t O[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) O[dt][v] = 0.0f;
+  half_t m_run = (half_t)(-__builtin_inff());
+  float l_star = 0.0f, inv_rho = 1.0f;
+  wait_async_copies();
+  __syncthreads();
+
+  for (int J = 0; J < tm.nJ; ++J) {
+    const uint8_t* cur = smem + (J & 1) * cbytes;
+    const ChunkStream cs{smem + ((J + 1) & 1) * cbytes, ws_base + (size_t)(J + 1 < tm.nJ ? J + 1 : J) * cbytes,
+                         wave_u};
+    if (tm.active && J <= jw_last) {
+      stream_piece<cbytes>(cs, 0);
+      f16v_t acc[2] = {};
+#pragma unroll
+      for (int kc = 0; kc < KC; ++kc)
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          const h8_t kf = *reinterpret_cast<const h8_t*>(cur + lay.k_op + ((size_t)(t * KC + kc) * 64 + lane) * 16);
+          acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf, qf[kc], acc[t], 0, 0, 0);
+        }
+      stream_piece<cbytes>(cs, 1);
+      h2_t s2[2][8];
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int v2 = 0; v2 < 8; ++v2) s2[t][v2] = scale2_to_f16(acc[t][2 * v2], acc[t][2 * v2 + 1], a.c);
+      if (64 * J + 63 > tm.qw) {
+        const half_t ninf = (half_t)(-__builtin_inff());
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+            if (64 * J + key_of(t, h, v) > qi) s2[t][v >> 1][v & 1] = ninf;
+      }
+      h2_t mx2 = hmax16(&s2[0][0]);
+      mx2 = hmax_halves(max_with_partner(mx2));
+      const h2_t mr2 = {m_run, m_run};
+      const h2_t mn2 = hmax2(mr2, mx2);
+      stream_piece<cbytes>(cs, 2);
+      h2_t p2[2][8];
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          h2_t xin[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) xin[i] = s2[t][4 * q + i] - mn2;
+          exp2_h2x4(xin, &p2[t][4 * q]);
+        }
+      const h2_t ra = exp2_h2(h2_t{mr2[0], mx2[0]} - mn2);
+      const float r = (float)ra[0];
+      const float A = (float)ra[1];
+      m_run = mn2[0];
+      float psum = 0.0f;
+      if (NORM == 1) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int v2 = 0; v2 < 8; ++v2)
+            psum = __builtin_amdgcn_fdot2(p2[t][v2], h2_t{(half_t)1, (half_t)1}, psum, false);
+        psum = add_with_partner(psum);
+      }
+      stream_piece<cbytes>(cs, 3);
+      uint8_t* dcodes = nullptr;
+      uint32_t* dmeta = nullptr;
+      if (DEBUG && row_ok) {
+        const size_t e = ((size_t)tm.hq * a.total_tokens + tm.t0 + qi) * a.NB + J;
+        dcodes = a.dbg_codes + e * 32;
+        dmeta = a.dbg_meta + e;
+      }
+      const PQuant pq = quantize_p_block<DEBUG>(p2, A, lane, h, dcodes, dmeta);
+      // deferred rescale (as in the HiFA4 kernel): O* = O / rho, l* = l / rho
+      if (__builtin_expect(J > 0 && __builtin_amdgcn_ballot_w64(r == 0.0f) != 0, 0)) {
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) O[dt][v] = r == 0.0f ? 0.0f : O[dt][v];
+        l_star = r == 0.0f ? 0.0f : l_star;
+      }
+      inv_rho = (r == 0.0f) ? 1.0f : inv_rho * __builtin_amdgcn_rcpf(r);
+      if (__builtin_expect(__builtin_amdgcn_ballot_w64(inv_rho > 0x1p64f) != 0, 0)) {
+        const float rho = __builtin_amdgcn_rcpf(inv_rho);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) O[dt][v] *= rho;
+        l_star *= rho;
+        inv_rho = 1.0f;
+      }
+      const float wp = 0.25f * pq.bval * inv_rho;
+      // B operand chunks of the 32x32x16 MFMA: c = 2t + jp holds the values of
+      // p2[t][4jp .. 4jp+3], i.e. operand slots 16t + 8jp + [0, 8)
+      h8_t pb[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pb[c][e] = pq.ov[8 * c + e];
+      if (NORM == 0) {
+        float osum = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          osum = __builtin_amdgcn_fdot2(h2_t{pq.ov[2 * i], pq.ov[2 * i + 1]}, h2_t{(half_t)1, (half_t)1}, osum, false);
+        l_star = __builtin_fmaf(add_with_partner(osum), wp, l_star);     // sum of P^ (exact before the scale)
+      } else {
+        l_star = __builtin_fmaf(psum, inv_rho, l_star);
+      }
+#pragma unroll
+      for (int dp = 0; dp < DT; dp += 2) {
+        f16v_t pv[2] = {};
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+#pragma unroll
+          for (int i = 0; i < 2; ++i) {
+            const h8_t vf =
+                *reinterpret_cast<const h8_t*>(cur + lay.v_op + ((size_t)((dp + i) * 4 + c) * 64 + lane) * 16);
+            pv[i] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pb[c], pv[i], 0, 0, 0);
+          }
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) O[dp + i][v] = __builtin_fmaf(pv[i][v], wp, O[dp + i][v]);
+        stream_piece<cbytes>(cs, 4 + dp / 2);
+      }
+      stream_pieces_from<cbytes>(cs, 4 + DT / 2);
+    } else {
+      stream_pieces_from<cbytes>(cs, 0);
+    }
+    wait_async_copies();
+    __syncthreads();
+  }
+  if (row_ok) {
+    const float inv = 1.0f / l_star;
+    half_t* dst = a.o + ((size_t)(tm.t0 + qi) * a.hq + tm.hq) * D;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        typedef _Float16 h4_t __attribute__((ext_vector_type(4)));
+        h4_t ov;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) ov[i] = (half_t)(O[dt][4 * j + i] * inv);
+        *reinterpret_cast<h4_t*>(dst + 32 * dt + 8 * j + 4 * h) = ov;
+      }
+    if (h == 0)
+      a.lse[(size_t)tm.hq * a.total_tokens + tm.t0 + qi] =
+          (float)m_run * 0.69314718055994531f + logf(l_star) - logf(inv_rho);
+  }
+}
+
+// ---------------------------------------------------------------------------
 template <typename K>
 static hipError_t launch_k(K kern, const AttnArgs& a, size_t lds, hipStream_t st) {
   const int grp = a.hq / a.hkv;
@@ -1002,8 +1214,25 @@ static hipError_t launch_k(K kern, const AttnArgs& a, size_t lds, hipStream_t st
   return hipGetLastError();
 }
 
-hipError_t launch_attention(const AttnArgs& a, int norm, bool fp16, bool qmean, hipStream_t st) {
-  if (fp16) {
+hipError_t launch_attention(const AttnArgs& a, int norm, int operands, bool qmean, hipStream_t st) {
+  if (operands == 2) {
+    const size_t lds = 2 * chunk_layout_fp16(a.D).bytes;
+    const bool dbg = a.dbg_codes != nullptr;
+#define HIFA4_PONLY(D)                                                                                      \
+  do {                                                                                                      \
+    if (norm == 0)                                                                                          \
+      return dbg ? launch_k(k_attn_ponly<D, 0, true>, a, lds, st) : launch_k(k_attn_ponly<D, 0, false>, a, lds, st); \
+    return dbg ? launch_k(k_attn_ponly<D, 1, true>, a, lds, st) : launch_k(k_attn_ponly<D, 1, false>, a, lds, st);   \
+  } while (0)
+    switch (a.D) {
+      case 64: HIFA4_PONLY(64);
+      case 128: HIFA4_PONLY(128);
+      case 256: HIFA4_PONLY(256);
+    }
+#undef HIFA4_PONLY
+    return hipErrorInvalidValue;
+  }
+  if (operands == 1) {
     const size_t lds = 2 * chunk_layout_fp16(a.D).bytes;
     switch (a.D) {
       case 64: return launch_k(k_attn_fp16<64>, a, lds, st);

@@ -75,6 +75,7 @@ hipError_t launch_prep_kv(const half_t* k, const half_t* v, const float* s, cons
 hipError_t launch_calib(const half_t* q, const half_t* k, int n, int S, int hq, int hkv, int D, uint32_t* stats,
                         unsigned long long* hist, hipStream_t st);
 hipError_t launch_selftest_exp2(const half_t* x, half_t* y, long n, hipStream_t st);
-hipError_t launch_attention(const AttnArgs& a, int norm, bool fp16, bool qmean, hipStream_t st);
+// operands: 0 HIF4, 1 FP16 reference, 2 P-only (fp16 Q, K, V; HIF4 P)
+hipError_t launch_attention(const AttnArgs& a, int norm, int operands, bool qmean, hipStream_t st);
 
 }  // namespace hifa4

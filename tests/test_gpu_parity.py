@@ -295,3 +295,59 @@ def test_qmean_qwen3_shape_sampled(h):
     rows = [0, 1, 63, 64, 2047, 4031, 4095]
     _say("qwen3 sampled q_mean")
     _run_and_compare(h, q, k, v, None, s, w.seqlen, heads=[0, 5, 31], rows=rows, q_mean=True)
+
+
+# ---------------------------------------------------------------------------
+# P-only local operator (Q, K, V fp16; only P quantized).  Its scores are fp32
+# sums in the MFMA's own order, so P^ codes are compared bit for bit on
+# integer-valued Q and K, where every partial sum is exact in fp32 and the
+# scores agree exactly with the oracle's; Gaussian inputs are checked
+# statistically (a score one fp16 ulp off can move one P^ code by one step).
+
+def _int_case(hq, hkv, d, lens, seed):
+    rng = np.random.default_rng(seed)
+    t = int(sum(lens))
+    q = rng.integers(-1, 2, size=(t, hq, d)).astype(np.float16)
+    k = rng.integers(-1, 2, size=(t, hkv, d)).astype(np.float16)
+    v = rng.standard_normal((t, hkv, d)).astype(np.float32).astype(np.float16)
+    return q, k, v, np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+
+
+def _run_ponly(h, q, k, v, cu, max_seqlen, norm, debug_p):
+    nm = h.NORM_PREORDER if norm == "preorder" else h.NORM_INCONSISTENT
+    return h.hifa4_attention_fwd(to_gpu(q), to_gpu(k), to_gpu(v), None, cu_seqlens=to_gpu(cu), max_seqlen=max_seqlen,
+                                 norm=nm, operands=h.OPERANDS_P_ONLY, debug_p=debug_p)
+
+
+@pytest.mark.parametrize("d,hq,hkv,lens", [(128, 4, 1, (300, 65, 1)), (64, 2, 2, (129, 200)), (256, 4, 2, (150,))])
+def test_p_only_exact_scores(h, d, hq, hkv, lens):
+    q, k, v, cu = _int_case(hq, hkv, d, lens, seed=d + hq)
+    for norm in ("preorder", "inconsistent"):
+        _say("p_only exact scores", d, hq, hkv, lens, norm)
+        res = _run_ponly(h, q, k, v, cu, max(lens), norm, True)
+        ref = oatt.attention_fwd(q, k, v, None, cu_seqlens=cu, operands="p_only", norm=norm, want_p=True)
+        o, lse = to_np(res[0]), to_np(res[1])
+        pc, pm = to_np(res[2]), to_np(res[3]).view(np.uint32)
+        for (b, hh), r in ref.items():
+            tok = cu[b] + r["rows"]
+            check_close(o[tok, hh], r["o"], what=f"p_only O seq {b} head {hh}")
+            check_close(lse[hh, tok], r["lse"], atol=2e-3, rtol=0, what="p_only LSE")
+            for ii, i in enumerate(r["rows"]):
+                nb_i = i // 64 + 1
+                assert np.array_equal(pc[hh, tok[ii], :nb_i], r["p_codes"][ii, :nb_i]), (b, hh, i)
+                assert np.array_equal(pm[hh, tok[ii], :nb_i], r["p_meta"][ii, :nb_i]), (b, hh, i)
+
+
+def test_p_only_gaussian(h):
+    q, k, v, cu = small_case(heads_q=4, heads_kv=2, head_dim=128, seqlens=(400, 77), seed=21)
+    for norm in ("preorder", "inconsistent"):
+        o, lse = _run_ponly(h, q, k, v, cu, 400, norm, False)
+        o, lse = to_np(o).astype(np.float64), to_np(lse)
+        ref = oatt.attention_fwd(q, k, v, None, cu_seqlens=cu, operands="p_only", norm=norm)
+        for (b, hh), r in ref.items():
+            tok = cu[b] + r["rows"]
+            g, w = o[tok, hh], r["o"]
+            cos = (g * w).sum(1) / (np.linalg.norm(g, axis=1) * np.linalg.norm(w, axis=1))
+            assert cos.min() > 0.999, (norm, b, hh, cos.min())
+            assert np.mean(np.abs(g - w) <= 2e-3 + 1e-2 * np.abs(w)) > 0.99
+            check_close(lse[hh, tok], r["lse"], atol=5e-3, rtol=1e-3, what="p_only LSE")

@@ -291,3 +291,37 @@ def test_scores_on_quantized_operands_match_exact_rounding():
                 wg = _rn32(Fraction(float(qf["scale"][i, g])) / 4 * c)
                 acc = _rn32(dg * wg) if acc is None else _rn32(dg * wg + acc)
             assert Fraction(float(s2[i, j])) == _rn16(acc), (i, j)
+
+
+def test_p_only_theorem1_and_constant_v():
+    """P-only local operator (Q, K, V unquantized fp16, only P quantized): the
+    setting of Theorem 1 itself.  One-block rows satisfy both closed forms
+    against the fp16 softmax weights a_j = P16_j and the raw V rows; a
+    constant V row is returned exactly under P-Reordering and scaled by
+    1 + eps under the inconsistent normalizer."""
+    q, k, v, cu = small_case(heads_q=1, heads_kv=1, seqlens=(64,), seed=12)
+    con = attention.attention_fwd(q, k, v, None, cu_seqlens=cu, operands="p_only", want_p=True)[(0, 0)]
+    mis = attention.attention_fwd(q, k, v, None, cu_seqlens=cu, operands="p_only", norm="inconsistent")[(0, 0)]
+    s2 = attention.scores_fp16(q[:, 0], k[:, 0], 128)
+    vrows = v[:, 0].astype(np.float64)
+    checked = 0
+    for i in range(8, 64):
+        keys = np.arange(i + 1)
+        a = attention.exp2_fp16(attention.sub_fp16(s2[i, keys], s2[i, keys].max())).astype(np.float64)
+        ahat = hif4.dequantize(hif4.unpack(con["p_codes"][i, 0], con["p_meta"][i, 0]))[: i + 1]
+        nz = a > 0
+        ostar, ebar, delta, w, e_t = _thm1_terms(a[nz], ahat[nz], vrows[keys][nz])
+        tol = 1e-12 * (1 + np.abs(ostar).max())
+        assert np.max(np.abs((con["o"][i] - ostar) - e_t / (1 + ebar))) < tol
+        assert np.max(np.abs((mis["o"][i] - ostar) - (e_t + ebar * ostar))) < tol
+        checked += 1
+    assert checked > 40
+    q, k, v, cu = small_case(heads_q=2, heads_kv=1, seqlens=(200,), seed=13)
+    v[:] = v[3, 0]
+    pre = attention.attention_fwd(q, k, v, None, cu_seqlens=cu, operands="p_only")
+    mis = attention.attention_fwd(q, k, v, None, cu_seqlens=cu, operands="p_only", norm="inconsistent")
+    for key in pre:
+        assert np.array_equal(pre[key]["o16"], np.broadcast_to(v[3, 0], pre[key]["o16"].shape))
+        ratio = pre[key]["l_con"] / pre[key]["l_mis"]
+        assert np.allclose(mis[key]["o"], ratio[:, None] * v[3, 0].astype(np.float64)[None, :], rtol=1e-12)
+        assert np.sum(np.abs(ratio - 1) > 1e-6) > 50
