@@ -6,6 +6,7 @@
 // after RoPE); Appendix C (GQA: s is per key-head channel).
 #include "hifa4_device.h"
 #include "hifa4_internal.h"
+#include "hifa4_packed.h"
 
 namespace hifa4 {
 
@@ -229,29 +230,46 @@ __global__ void __launch_bounds__(512) k_prep_kv_hif4(const half_t* __restrict__
   const ChunkLayout lay = chunk_layout_hif4(G, qmean);
   uint8_t* chunk = ws + ((size_t)(b * heads_kv + hk) * NB + J) * lay.bytes;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, h = lane >> 5;
-  float x[32], o[32];
   if (!is_v) {
-    // this head's smoothing scales and their reciprocals (one division per
-    // channel), staged in LDS
-    float* rs = reinterpret_cast<float*>(sm);
-    float* ss = rs + D;
+    const int t = wave / G, g = wave % G;
+    const int key = 32 * t + (lane & 31);
+    const int pos = 64 * J + key;
+    // the key's 32 channels 64g + 32h + [0, 32) as 16 fp16 pairs, requested
+    // before the smoothing scales are staged so that both loads overlap
+    h2_t x[16];
+    if (pos < L) {
+      typedef uint32_t u4v_t __attribute__((ext_vector_type(4)));
+      const u4v_t* src = reinterpret_cast<const u4v_t*>(k + ((size_t)(t0 + pos) * heads_kv + hk) * D + 64 * g + 32 * h);
+#pragma unroll
+      for (int v4 = 0; v4 < 4; ++v4) {
+        const u4v_t w = src[v4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const uint32_t wi = w[i];     // copy first: bit-casting an ext_vector element in place misreads it
+          x[4 * v4 + i] = __builtin_bit_cast(h2_t, wi);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) x[i] = h2_t{(half_t)0, (half_t)0};
+    }
     if (s) {
+      // this head's smoothing scales and their reciprocals (one division per
+      // channel), staged in LDS; then k~ = fp16(k/s) per element
+      float* rs = reinterpret_cast<float*>(sm);
+      float* ss = rs + D;
       for (int c = threadIdx.x; c < D; c += blockDim.x) {
         const float sc = s[(size_t)hk * D + c];
         ss[c] = sc;
         rs[c] = 1.0f / sc;
       }
       __syncthreads();
-    }
-    const int t = wave / G, g = wave % G;
-    const int key = 32 * t + (lane & 31);
-    const int pos = 64 * J + key;
-    if (pos < L) {
-      const half_t* src = k + ((size_t)(t0 + pos) * heads_kv + hk) * D + 64 * g + 32 * h;
-      load_smoothed32<true>(src, s ? ss + 64 * g + 32 * h : nullptr, x, rs + 64 * g + 32 * h);
-    } else {
+      const float* sc = ss + 64 * g + 32 * h;
+      const float* rc = rs + 64 * g + 32 * h;
 #pragma unroll
-      for (int c = 0; c < 32; ++c) x[c] = 0.0f;
+      for (int i = 0; i < 16; ++i)
+        x[i] = h2_t{div_rn16_rcp((float)x[i][0], sc[2 * i], rc[2 * i]),
+                    div_rn16_rcp((float)x[i][1], sc[2 * i + 1], rc[2 * i + 1])};
     }
     if (qmean) {
       // Q-Mean key sums (Algorithm 1's correction term): the exact sum of the
@@ -259,7 +277,7 @@ __global__ void __launch_bounds__(512) k_prep_kv_hif4(const half_t* __restrict__
       // one partial per (32-key half, group) in LDS, then rounded once to fp32.
       double part = 0.0;
 #pragma unroll
-      for (int c = 0; c < 32; ++c) part += (double)x[c];
+      for (int i = 0; i < 16; ++i) part += (double)(float)x[i][0] + (double)(float)x[i][1];
       part += __shfl_xor(part, 32);
       double* parts = reinterpret_cast<double*>(sm + 2 * D * sizeof(float));     // [2][G][32]
       if (h == 0) parts[(t * G + g) * 32 + (lane & 31)] = part;
@@ -270,14 +288,10 @@ __global__ void __launch_bounds__(512) k_prep_kv_hif4(const half_t* __restrict__
         reinterpret_cast<float*>(chunk + lay.kappa)[32 * t + (lane & 31)] = (float)sum;
       }
     }
-    const GroupMeta gm = quantize_split<kRows>(x, o, h);
-    h32_t hv;
-#pragma unroll
-    for (int c = 0; c < 32; ++c) hv[c] = (half_t)o[c];
-    const i6_t pk = __builtin_amdgcn_cvt_scalef32_pk32_fp6_f16(hv, 1.0f);
-    store_split_operand(chunk + lay.k_op + (size_t)(t * G + g) * 2 * kOpRecord, lane, pk, gm.base);
+    const GroupOps go = rows_quantize(x);
+    store_split_operand(chunk + lay.k_op + (size_t)(t * G + g) * 2 * kOpRecord, lane, go.pk, go.base);
     if (h == 0)
-      reinterpret_cast<uint32_t*>(chunk + lay.k_scale)[(t * G + g) * 32 + (lane & 31)] = split_scale_word(gm.base);
+      reinterpret_cast<uint32_t*>(chunk + lay.k_scale)[(t * G + g) * 32 + (lane & 31)] = split_scale_word(go.base);
   } else {
     // stage V rows [64J, 64J+64) of this head, zero past the sequence end
     half_t* vt = reinterpret_cast<half_t*>(sm);        // [64 keys][D]
@@ -292,21 +306,19 @@ __global__ void __launch_bounds__(512) k_prep_kv_hif4(const half_t* __restrict__
     __syncthreads();
     const int dt = wave;
     const int d = 32 * dt + (lane & 31);
-    // slot s = 4kk + i holds key 32t + 8j + 4h + i of the lane's 4-block
-    // kk = (t, j), which is the quantizer's block order as well
+    // the lane's 32 keys in the order of the attention kernel's P^ operand:
+    // x[t][v2] = keys 32t + 8(v2/2) + 4h + 2(v2%2) + {0, 1} of channel d
+    h2_t x[2][8];
 #pragma unroll
-    for (int kk = 0; kk < 8; ++kk) {
-      const int t = kk >> 2, j = kk & 3;
+    for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) x[4 * kk + i] = (float)vt[(32 * t + 8 * j + 4 * h + i) * D + d];
-    }
-    const GroupMeta gm = quantize_split<kKeys>(x, o, h);
-    h32_t hv;
-#pragma unroll
-    for (int c = 0; c < 32; ++c) hv[c] = (half_t)o[c];
-    const i6_t pk = __builtin_amdgcn_cvt_scalef32_pk32_fp6_f16(hv, 1.0f);
-    store_split_operand(chunk + lay.v_op + (size_t)dt * 2 * kOpRecord, lane, pk, gm.base);
-    if (h == 0) reinterpret_cast<uint32_t*>(chunk + lay.v_scale)[d] = split_scale_word(gm.base);
+      for (int v2 = 0; v2 < 8; ++v2) {
+        const int k0 = 32 * t + 8 * (v2 >> 1) + 4 * h + 2 * (v2 & 1);
+        x[t][v2] = h2_t{vt[k0 * D + d], vt[(k0 + 1) * D + d]};
+      }
+    const GroupOps go = keys_quantize(x, lane, h);
+    store_split_operand(chunk + lay.v_op + (size_t)dt * 2 * kOpRecord, lane, go.pk, go.base);
+    if (h == 0) reinterpret_cast<uint32_t*>(chunk + lay.v_scale)[d] = split_scale_word(go.base);
   }
 }
 
