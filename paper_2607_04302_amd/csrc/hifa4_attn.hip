@@ -263,6 +263,10 @@ __device__ __forceinline__ void load_q_half_group(const half_t* __restrict__ src
     const float4* s4 = reinterpret_cast<const float4*>(sp);
 #pragma unroll
     for (int v = 0; v < 8; ++v) r.s[v] = s4[v];
+  } else {
+    // defined on every path, so that no undefined value is carried anywhere
+#pragma unroll
+    for (int v = 0; v < 8; ++v) r.s[v] = make_float4(1.0f, 1.0f, 1.0f, 1.0f);
   }
 }
 
