@@ -278,11 +278,15 @@ def main():
     if w.alpha > 0:
         src = WORKLOADS[w.calib_from] if w.calib_from else w
         qc, kc = make_calibration(src)
-        s, rep = h.hifa4_calibrate_smooth_qk(torch.from_numpy(qc).to(dev), torch.from_numpy(kc).to(dev), w.alpha)
-        del qc, kc
+        qcd, kcd = torch.from_numpy(qc).to(dev), torch.from_numpy(kc).to(dev)
+        torch.cuda.synchronize()
+        tc = time.perf_counter()
+        s, rep = h.hifa4_calibrate_smooth_qk(qcd, kcd, w.alpha)     # synchronizes
+        tc = time.perf_counter() - tc
+        del qc, kc, qcd, kcd
         sn = s.cpu().numpy()
         calib = {"n_calib": len(src.calib_seeds), "alpha": w.alpha, "rho_k": round(rep["rho_k"], 3),
-                 "t_kq": round(rep["t_kq"], 3)}
+                 "t_kq": round(rep["t_kq"], 3), "seconds": round(tc, 4)}
     torch.cuda.synchronize()
     flops = w.flops()
     ws = h.Workspace()

@@ -177,6 +177,22 @@ hifa4_status hifa4_calibrate_smooth_qk(const hifa4_problem* p, int32_t n_calib,
                                        void* workspace, size_t workspace_bytes,
                                        void* stream);
 
+/* Offline calibration of several layers in one call (Sections 4.3-4.4 and
+ * Appendix F: the statistics, the scale and the gate decision are taken per
+ * layer).  Layer l reads q_calib + l * (n_calib*max_seqlen*num_heads_q*head_dim)
+ * and k_calib + l * (n_calib*max_seqlen*num_heads_kv*head_dim) fp16 elements
+ * (DEVICE, layers stacked on a leading axis) and writes s_out + l*num_heads_kv*
+ * head_dim (DEVICE fp32) and reports[l] (HOST, may be NULL); each layer is
+ * exactly hifa4_calibrate_smooth_qk on its slice, with the same alpha (alpha < 0
+ * lets the gate decide per layer).  workspace: DEVICE, at least
+ * hifa4_calibrate_workspace_bytes(p, n_calib), reused by every layer.
+ * Synchronizes `stream`.  On an error no later layer is processed. */
+hifa4_status hifa4_calibrate_smooth_qk_layers(const hifa4_problem* p, int32_t n_layers,
+                                              int32_t n_calib, const void* q_calib,
+                                              const void* k_calib, float alpha, float* s_out,
+                                              hifa4_calib_report* reports, void* workspace,
+                                              size_t workspace_bytes, void* stream);
+
 /* Smooth-QK then HIF4 quantization of Q~ = fp16(fp32(q)*s) and
  * K~ = fp16(fp32(k)/s) (IEEE single multiply / correctly rounded divide, one
  * rounding to fp16), in groups of 64 consecutive channels of each (token,

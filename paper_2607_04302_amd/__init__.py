@@ -7,7 +7,7 @@ directory and a missing or stale build raises immediately -- there is no
 fallback implementation.
 
 Names mirror the C entry points:
-  hifa4_calibrate_smooth_qk, hifa4_quantize_qk, hifa4_quantize_v,
+  hifa4_calibrate_smooth_qk, hifa4_calibrate_smooth_qk_layers, hifa4_quantize_qk, hifa4_quantize_v,
   hifa4_attention_fwd, hifa4_workspace_bytes, hifa4_selftest_exp2,
   hifa4_last_error.
 """
@@ -27,6 +27,7 @@ STATUS = {0: "HIFA4_OK", -1: "HIFA4_ERR_INVALID_ARGUMENT", -2: "HIFA4_ERR_UNSUPP
           -3: "HIFA4_ERR_WORKSPACE", -4: "HIFA4_ERR_HIP"}
 
 EXPORTED = ("hifa4_workspace_bytes", "hifa4_calibrate_workspace_bytes", "hifa4_calibrate_smooth_qk",
+            "hifa4_calibrate_smooth_qk_layers",
             "hifa4_quantize_qk", "hifa4_quantize_v", "hifa4_attention_fwd", "hifa4_selftest_exp2",
             "hifa4_last_error")
 
@@ -74,6 +75,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.hifa4_calibrate_smooth_qk.restype = ctypes.c_int
     lib.hifa4_calibrate_smooth_qk.argtypes = [P(Problem), ctypes.c_int32, vp, vp, ctypes.c_float, vp,
                                               P(CalibReport), vp, sz, vp]
+    lib.hifa4_calibrate_smooth_qk_layers.restype = ctypes.c_int
+    lib.hifa4_calibrate_smooth_qk_layers.argtypes = [P(Problem), ctypes.c_int32, ctypes.c_int32, vp, vp,
+                                                     ctypes.c_float, vp, P(CalibReport), vp, sz, vp]
     lib.hifa4_quantize_qk.restype = ctypes.c_int
     lib.hifa4_quantize_qk.argtypes = [P(Problem), vp, vp, vp, vp, vp, vp, vp, vp]
     lib.hifa4_quantize_v.restype = ctypes.c_int
@@ -180,6 +184,27 @@ def hifa4_calibrate_smooth_qk(q_cal, k_cal, alpha: float):
                                          _ptr(out), ctypes.byref(rep), _ptr(ws), ws_bytes,
                                          _stream(q_cal.device)), "hifa4_calibrate_smooth_qk")
     return out, {"rho_k": rep.rho_k, "t_kq": rep.t_kq, "branch": rep.branch, "alpha_used": rep.alpha_used}
+
+
+def hifa4_calibrate_smooth_qk_layers(q_cal, k_cal, alpha: float):
+    """q_cal [L, n, S, Hq, D], k_cal [L, n, S, Hkv, D] fp16 on the GPU (L
+    layers).  Returns (s fp32 [L, Hkv, D] on the GPU, list of L report dicts).
+    Synchronizes the stream."""
+    torch = _torch()
+    _require(q_cal, torch.float16, "q_cal")
+    _require(k_cal, torch.float16, "k_cal")
+    lib = load_library()
+    n_layers, n, s, hq, d = q_cal.shape
+    hkv = k_cal.shape[3]
+    p = Problem(1, hq, hkv, d, s, None, 0, 1)
+    ws_bytes = int(lib.hifa4_calibrate_workspace_bytes(ctypes.byref(p), n))
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=q_cal.device)
+    out = torch.empty((n_layers, hkv, d), dtype=torch.float32, device=q_cal.device)
+    reps = (CalibReport * n_layers)()
+    _check(lib.hifa4_calibrate_smooth_qk_layers(ctypes.byref(p), n_layers, n, _ptr(q_cal), _ptr(k_cal),
+                                                float(alpha), _ptr(out), reps, _ptr(ws), ws_bytes,
+                                                _stream(q_cal.device)), "hifa4_calibrate_smooth_qk_layers")
+    return out, [{"rho_k": r.rho_k, "t_kq": r.t_kq, "branch": r.branch, "alpha_used": r.alpha_used} for r in reps]
 
 
 def hifa4_quantize_qk(q, k, s=None, cu_seqlens=None, max_seqlen=None):

@@ -279,4 +279,27 @@ hifa4_status hifa4_calibrate_smooth_qk(const hifa4_problem* p, int32_t n_calib, 
   return HIFA4_OK;
 }
 
+hifa4_status hifa4_calibrate_smooth_qk_layers(const hifa4_problem* p, int32_t n_layers, int32_t n_calib,
+                                              const void* q_calib, const void* k_calib, float alpha, float* s_out,
+                                              hifa4_calib_report* reports, void* workspace, size_t workspace_bytes,
+                                              void* stream) {
+  if (!p) return fail(HIFA4_ERR_INVALID_ARGUMENT, "problem is NULL");
+  if (n_layers <= 0) return fail(HIFA4_ERR_INVALID_ARGUMENT, "n_layers must be > 0");
+  if (!q_calib || !k_calib || !s_out) return fail(HIFA4_ERR_INVALID_ARGUMENT, "null tensor pointer");
+  if (n_calib <= 0 || p->max_seqlen <= 0) return fail(HIFA4_ERR_INVALID_ARGUMENT, "n_calib and max_seqlen must be > 0");
+  const size_t q_layer = (size_t)n_calib * p->max_seqlen * p->num_heads_q * p->head_dim;
+  const size_t k_layer = (size_t)n_calib * p->max_seqlen * p->num_heads_kv * p->head_dim;
+  const size_t s_layer = (size_t)p->num_heads_kv * p->head_dim;
+  for (int32_t l = 0; l < n_layers; ++l) {
+    const hifa4_status st = hifa4_calibrate_smooth_qk(
+        p, n_calib, (const uint16_t*)q_calib + l * q_layer, (const uint16_t*)k_calib + l * k_layer, alpha,
+        s_out + l * s_layer, reports ? reports + l : nullptr, workspace, workspace_bytes, stream);
+    if (st != HIFA4_OK) {
+      const std::string msg = g_last_error;
+      return fail(st, "layer %d: %s", l, msg.c_str());
+    }
+  }
+  return HIFA4_OK;
+}
+
 }  // extern "C"

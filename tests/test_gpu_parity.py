@@ -351,3 +351,35 @@ def test_p_only_gaussian(h):
             assert cos.min() > 0.999, (norm, b, hh, cos.min())
             assert np.mean(np.abs(g - w) <= 2e-3 + 1e-2 * np.abs(w)) > 0.99
             check_close(lse[hh, tok], r["lse"], atol=5e-3, rtol=1e-3, what="p_only LSE")
+
+
+def _calib_layer(rng, k_sigma, q_sigma, outlier, n=4, S=256, hq=4, hkv=1, d=128):
+    q = (rng.standard_normal((n, S, hq, d)) * q_sigma).astype(np.float16)
+    k = rng.standard_normal((n, S, hkv, d)) * k_sigma
+    if outlier:
+        k[..., 7] *= outlier          # one channel of 128: under 1% of K's elements
+    return q, k.astype(np.float16)
+
+
+def test_calibration_layers(h):
+    """Per-layer calibration in one call (the gate decides per layer): three
+    layers built so that the literal gate picks Strong (one x12 outlier
+    channel, T ~ 7), Mild (the same outlier with a wider Q, T ~ 2.7) and
+    Bypass (no outlier); every layer's scales and report equal the oracle's
+    single-layer calibration."""
+    rng = np.random.default_rng(77)
+    layers = [_calib_layer(rng, 1.0, 1.0, 12.0), _calib_layer(rng, 0.1, 0.35, 12.0), _calib_layer(rng, 1.0, 1.0, 0)]
+    qs = np.stack([l[0] for l in layers])
+    ks = np.stack([l[1] for l in layers])
+    s_gpu, reps = h.hifa4_calibrate_smooth_qk_layers(to_gpu(qs), to_gpu(ks), -1.0)
+    s_gpu = to_np(s_gpu)
+    branches = []
+    for i, (q, k) in enumerate(layers):
+        s_ref, rep = osmooth.calibrate(q, k, 1, -1.0)
+        ulp = np.abs(s_gpu[i].view(np.int32).astype(np.int64) - s_ref.view(np.int32).astype(np.int64))
+        assert ulp.max() <= 1, i
+        assert reps[i]["branch"] == rep["branch"], i
+        assert abs(reps[i]["rho_k"] - rep["rho_k"]) < 1e-9 * rep["rho_k"]
+        assert abs(reps[i]["t_kq"] - rep["t_kq"]) < 1e-12 * rep["t_kq"]
+        branches.append(rep["branch"])
+    assert branches == [2, 1, 0]
