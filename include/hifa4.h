@@ -202,7 +202,10 @@ hifa4_status hifa4_calibrate_smooth_qk_layers(const hifa4_problem* p, int32_t n_
  * Outputs (DEVICE, canonical layout):
  *   q_codes uint8 [T, num_heads_q, head_dim/64, 32], q_meta uint32 [T, Hq, D/64]
  *   k_codes uint8 [T, num_heads_kv, head_dim/64, 32], k_meta uint32 [T, Hkv, D/64]
- * where T is the token count.  Asynchronous. */
+ * where T is the token count.  q, q_codes and q_meta may all be NULL: then
+ * only K^ is written (filling or appending to a K^ cache; rows are
+ * independent, so the K^ of new tokens can be written in place at their
+ * cache rows).  Asynchronous. */
 hifa4_status hifa4_quantize_qk(const hifa4_problem* p, const void* q, const void* k,
                                const float* s, void* q_codes, void* q_meta,
                                void* k_codes, void* k_meta, void* stream);
@@ -239,6 +242,39 @@ hifa4_status hifa4_attention_fwd(const hifa4_problem* p, const hifa4_fwd_options
                                  const void* q, const void* k, const void* v,
                                  const float* s, void* o, float* lse,
                                  void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace size in bytes of hifa4_decode_fwd for problem p (0 if p is
+ * invalid).  It grows with batch * num_heads_q * ceil(max_seqlen/64). */
+size_t hifa4_decode_workspace_bytes(const hifa4_problem* p);
+
+/* One decode step of HiFA4 over a packed HIF4 K/V cache: for each sequence b,
+ * the attention of its newest token (position L_b - 1, which sees every cached
+ * key) -- row L_b - 1 of hifa4_attention_fwd on the same sequence, computed
+ * from the cache.  The paper evaluates prefill only and leaves decode and
+ * the KV-cache footprint open; this entry point applies Algorithm 1 and
+ * Section 4.5 to that row with the same contract, including every P^ code.
+ * p describes the cached sequences (their lengths include the newest token):
+ * BSHD (every length max_seqlen) or THD with cu_seqlens; causal must be 1.
+ * q: DEVICE fp16 [batch, num_heads_q, head_dim], the raw query of each
+ *    sequence's newest token (smoothed here with s when opt->smooth_qk);
+ * k_codes/k_meta: DEVICE canonical K^ cache [T, Hkv, D/64, 32] / [T, Hkv, D/64]
+ *    as written by hifa4_quantize_qk with the same s (T the token count);
+ * v_codes/v_meta: DEVICE canonical V^ cache [batch, NB, Hkv, D, 32] /
+ *    [batch, NB, Hkv, D] as written by hifa4_quantize_v (NB = ceil(max_seqlen/64));
+ * o: DEVICE fp16 [batch, num_heads_q, head_dim]; lse: DEVICE fp32
+ *    [num_heads_q, batch]; rows of empty sequences are left untouched.
+ * opt: norm, smooth_qk, debug_p_codes/_meta ([num_heads_q, batch, NB, 32] /
+ *    [num_heads_q, batch, NB], entries J < ceil(L_b/64) written) and
+ *    timing_events (before the query quantization, after the score kernel,
+ *    after the merge) as for hifa4_attention_fwd; operands must be
+ *    HIFA4_OPERANDS_HIF4 and q_mean 0 (the cache carries no key sums), else
+ *    HIFA4_ERR_UNSUPPORTED; num_heads_q / num_heads_kv must be <= 8.
+ * workspace: DEVICE, >= hifa4_decode_workspace_bytes(p).  Asynchronous. */
+hifa4_status hifa4_decode_fwd(const hifa4_problem* p, const hifa4_fwd_options* opt,
+                              const void* q, const void* k_codes, const void* k_meta,
+                              const void* v_codes, const void* v_meta, const float* s,
+                              void* o, float* lse, void* workspace, size_t workspace_bytes,
+                              void* stream);
 
 /* Device self-test of the kernels' fp16 exponential: y[i] = fp16(2^x[i]) for
  * n fp16 inputs x (DEVICE, fp16 bits), evaluated by the same device routine

@@ -8,8 +8,8 @@ fallback implementation.
 
 Names mirror the C entry points:
   hifa4_calibrate_smooth_qk, hifa4_calibrate_smooth_qk_layers, hifa4_quantize_qk, hifa4_quantize_v,
-  hifa4_attention_fwd, hifa4_workspace_bytes, hifa4_selftest_exp2,
-  hifa4_last_error.
+  hifa4_attention_fwd, hifa4_workspace_bytes, hifa4_decode_fwd,
+  hifa4_decode_workspace_bytes, hifa4_selftest_exp2, hifa4_last_error.
 """
 from __future__ import annotations
 
@@ -28,8 +28,8 @@ STATUS = {0: "HIFA4_OK", -1: "HIFA4_ERR_INVALID_ARGUMENT", -2: "HIFA4_ERR_UNSUPP
 
 EXPORTED = ("hifa4_workspace_bytes", "hifa4_calibrate_workspace_bytes", "hifa4_calibrate_smooth_qk",
             "hifa4_calibrate_smooth_qk_layers",
-            "hifa4_quantize_qk", "hifa4_quantize_v", "hifa4_attention_fwd", "hifa4_selftest_exp2",
-            "hifa4_last_error")
+            "hifa4_quantize_qk", "hifa4_quantize_v", "hifa4_attention_fwd", "hifa4_decode_workspace_bytes",
+            "hifa4_decode_fwd", "hifa4_selftest_exp2", "hifa4_last_error")
 
 
 class Problem(ctypes.Structure):
@@ -84,6 +84,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.hifa4_quantize_v.argtypes = [P(Problem), vp, vp, vp, vp]
     lib.hifa4_attention_fwd.restype = ctypes.c_int
     lib.hifa4_attention_fwd.argtypes = [P(Problem), P(FwdOptions), vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.hifa4_decode_workspace_bytes.restype = sz
+    lib.hifa4_decode_workspace_bytes.argtypes = [P(Problem)]
+    lib.hifa4_decode_fwd.restype = ctypes.c_int
+    lib.hifa4_decode_fwd.argtypes = [P(Problem), P(FwdOptions), vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.hifa4_selftest_exp2.restype = ctypes.c_int
     lib.hifa4_selftest_exp2.argtypes = [vp, vp, ctypes.c_int64, vp]
     lib.hifa4_last_error.restype = ctypes.c_char_p
@@ -210,17 +214,20 @@ def hifa4_calibrate_smooth_qk_layers(q_cal, k_cal, alpha: float):
 def hifa4_quantize_qk(q, k, s=None, cu_seqlens=None, max_seqlen=None):
     """Canonical HIF4 codes of Smooth-QK'd Q and K.  Returns (q_codes uint8
     [T,Hq,D/64,32], q_meta int32 [T,Hq,D/64], k_codes, k_meta) -- meta words
-    are uint32 bit patterns held in int32 tensors."""
+    are uint32 bit patterns held in int32 tensors.  q=None quantizes K only
+    (q_codes and q_meta are then None)."""
     torch = _torch()
     _require(q, torch.float16, "q")
     _require(k, torch.float16, "k")
     _require(s, torch.float32, "s")
-    sh = shape_of(q, k, cu_seqlens, max_seqlen)
+    sh = shape_of(k if q is None else q, k, cu_seqlens, max_seqlen)
     lib = load_library()
     g = sh.head_dim // 64
-    dev = q.device
-    qc = torch.empty((sh.tokens, sh.heads_q, g, 32), dtype=torch.uint8, device=dev)
-    qm = torch.empty((sh.tokens, sh.heads_q, g), dtype=torch.int32, device=dev)
+    dev = k.device
+    qc = qm = None
+    if q is not None:
+        qc = torch.empty((sh.tokens, sh.heads_q, g, 32), dtype=torch.uint8, device=dev)
+        qm = torch.empty((sh.tokens, sh.heads_q, g), dtype=torch.int32, device=dev)
     kc = torch.empty((sh.tokens, sh.heads_kv, g, 32), dtype=torch.uint8, device=dev)
     km = torch.empty((sh.tokens, sh.heads_kv, g), dtype=torch.int32, device=dev)
     p = sh.problem()
@@ -298,6 +305,79 @@ def hifa4_attention_fwd(q, k, v, s=None, cu_seqlens=None, max_seqlen=None, norm:
     ws = (workspace or _default_ws).get(need, dev)
     _check(lib.hifa4_attention_fwd(ctypes.byref(p), ctypes.byref(opt), _ptr(q), _ptr(k), _ptr(v), _ptr(s),
                                    _ptr(o), _ptr(l), _ptr(ws), ws.numel(), _stream(dev)), "hifa4_attention_fwd")
+    if debug_p:
+        return o, l, pc, pm
+    return o, l
+
+
+def decode_shape(q, k_codes, cu_seqlens=None, max_seqlen=None) -> Shape:
+    """Problem shape of a decode step: q [B, Hq, D], K^ cache codes
+    [T, Hkv, D/64, 32] (T = B * max_seqlen without cu_seqlens)."""
+    if q.dim() != 3 or k_codes.dim() != 4:
+        raise ValueError("decode takes q [batch, heads, dim] and k_codes [tokens, heads_kv, dim/64, 32]")
+    b, hq, d = q.shape
+    t, hkv = k_codes.shape[0], k_codes.shape[1]
+    if cu_seqlens is None:
+        if t % b:
+            raise ValueError("without cu_seqlens the cache holds batch * max_seqlen tokens")
+        return Shape(b, hq, hkv, d, t // b, t)
+    if max_seqlen is None:
+        raise ValueError("max_seqlen is required with cu_seqlens")
+    _require(cu_seqlens, _torch().int32, "cu_seqlens")
+    if cu_seqlens.numel() != b + 1:
+        raise ValueError("cu_seqlens must hold batch + 1 entries")
+    return Shape(b, hq, hkv, d, int(max_seqlen), t, cu_seqlens)
+
+
+def hifa4_decode_workspace_bytes(shape: Shape) -> int:
+    p = shape.problem()
+    return int(load_library().hifa4_decode_workspace_bytes(ctypes.byref(p)))
+
+
+def hifa4_decode_fwd(q, k_codes, k_meta, v_codes, v_meta, s=None, cu_seqlens=None, max_seqlen=None,
+                     norm: int = NORM_PREORDER, smooth_qk: Optional[bool] = None, debug_p: bool = False,
+                     out=None, lse=None, workspace: Optional[Workspace] = None, timing_events=None):
+    """One decode step over a packed HIF4 cache: q [B, Hq, D] fp16 is the query
+    of each sequence's newest token; the cache is the output of
+    hifa4_quantize_qk (K^, same s) and hifa4_quantize_v (V^) over the cached
+    sequences.  Returns (o [B, Hq, D], lse [Hq, B]) or, with debug_p,
+    (o, lse, p_codes uint8 [Hq, B, NB, 32], p_meta int32 [Hq, B, NB])."""
+    torch = _torch()
+    _require(q, torch.float16, "q")
+    _require(k_codes, torch.uint8, "k_codes")
+    _require(k_meta, torch.int32, "k_meta")
+    _require(v_codes, torch.uint8, "v_codes")
+    _require(v_meta, torch.int32, "v_meta")
+    _require(s, torch.float32, "s")
+    sh = decode_shape(q, k_codes, cu_seqlens, max_seqlen)
+    nb = (sh.max_seqlen + 63) // 64
+    g = sh.head_dim // 64
+    if tuple(k_meta.shape) != (sh.tokens, sh.heads_kv, g) or tuple(k_codes.shape[2:]) != (g, 32):
+        raise ValueError("k_codes/k_meta do not match [tokens, heads_kv, dim/64(, 32)]")
+    if tuple(v_codes.shape) != (sh.batch, nb, sh.heads_kv, sh.head_dim, 32) or \
+            tuple(v_meta.shape) != (sh.batch, nb, sh.heads_kv, sh.head_dim):
+        raise ValueError("v_codes/v_meta do not match [batch, NB, heads_kv, dim(, 32)]")
+    lib = load_library()
+    dev = q.device
+    if smooth_qk is None:
+        smooth_qk = s is not None
+    o = torch.empty_like(q) if out is None else out
+    l = torch.empty((sh.heads_q, sh.batch), dtype=torch.float32, device=dev) if lse is None else lse
+    pc = pm = None
+    if debug_p:
+        pc = torch.zeros((sh.heads_q, sh.batch, nb, 32), dtype=torch.uint8, device=dev)
+        pm = torch.zeros((sh.heads_q, sh.batch, nb), dtype=torch.int32, device=dev)
+    ev_arr = None
+    if timing_events is not None:
+        ev_arr = (ctypes.c_void_p * 3)(*[e.cuda_event for e in timing_events])
+    opt = FwdOptions(norm, OPERANDS_HIF4, 1 if smooth_qk else 0, _ptr(pc), _ptr(pm),
+                     ctypes.cast(ev_arr, ctypes.c_void_p) if ev_arr is not None else None, 0)
+    p = sh.problem()
+    need = int(lib.hifa4_decode_workspace_bytes(ctypes.byref(p)))
+    ws = (workspace or _default_ws).get(need, dev)
+    _check(lib.hifa4_decode_fwd(ctypes.byref(p), ctypes.byref(opt), _ptr(q), _ptr(k_codes), _ptr(k_meta),
+                                _ptr(v_codes), _ptr(v_meta), _ptr(s), _ptr(o), _ptr(l), _ptr(ws), ws.numel(),
+                                _stream(dev)), "hifa4_decode_fwd")
     if debug_p:
         return o, l, pc, pm
     return o, l

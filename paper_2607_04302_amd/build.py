@@ -12,7 +12,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libhifa4.so")
-SOURCES = ["hifa4_api.cpp", "hifa4_quant.hip", "hifa4_attn.hip"]
+SOURCES = ["hifa4_api.cpp", "hifa4_quant.hip", "hifa4_attn.hip", "hifa4_decode.hip"]
 
 
 def hipcc() -> str:

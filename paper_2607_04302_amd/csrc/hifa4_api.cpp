@@ -84,13 +84,17 @@ hifa4_status hifa4_quantize_qk(const hifa4_problem* p, const void* q, const void
   Dims d;
   hifa4_status st = check_problem(p, &d);
   if (st != HIFA4_OK) return st;
-  if (!q || !k || !q_codes || !q_meta || !k_codes || !k_meta)
+  const bool q_none = !q && !q_codes && !q_meta;
+  if ((!q_none && (!q || !q_codes || !q_meta)) || !k || !k_codes || !k_meta)
     return fail(HIFA4_ERR_INVALID_ARGUMENT, "null tensor pointer");
   hipStream_t hs = (hipStream_t)stream;
   using hifa4::half_t;
-  hipError_t e = hifa4::launch_quant_rows((const half_t*)q, s, (uint8_t*)q_codes, (uint32_t*)q_meta, d.tokens,
-                                          p->num_heads_q, p->num_heads_kv, p->head_dim, false, hs);
-  if (e != hipSuccess) return hip_fail(e, "quantize Q");
+  hipError_t e = hipSuccess;
+  if (!q_none) {
+    e = hifa4::launch_quant_rows((const half_t*)q, s, (uint8_t*)q_codes, (uint32_t*)q_meta, d.tokens,
+                                 p->num_heads_q, p->num_heads_kv, p->head_dim, false, hs);
+    if (e != hipSuccess) return hip_fail(e, "quantize Q");
+  }
   e = hifa4::launch_quant_rows((const half_t*)k, s, (uint8_t*)k_codes, (uint32_t*)k_meta, d.tokens, p->num_heads_kv,
                                p->num_heads_kv, p->head_dim, true, hs);
   if (e != hipSuccess) return hip_fail(e, "quantize K");
@@ -162,6 +166,69 @@ hifa4_status hifa4_attention_fwd(const hifa4_problem* p, const hifa4_fwd_options
   a.c = (float)(1.4426950408889634 / std::sqrt((double)p->head_dim));
   e = hifa4::launch_attention(a, opt->norm, opt->operands, qmean, hs);
   if (e != hipSuccess) return hip_fail(e, "attention kernel");
+  if (ev && (e = hipEventRecord(ev[2], hs)) != hipSuccess) return hip_fail(e, "timing event");
+  return HIFA4_OK;
+}
+
+size_t hifa4_decode_workspace_bytes(const hifa4_problem* p) {
+  Dims d;
+  if (check_problem(p, &d) != HIFA4_OK) return 0;
+  return hifa4::decode_workspace_bytes(p->batch, p->num_heads_q, p->head_dim, std::max(1, d.NB));
+}
+
+hifa4_status hifa4_decode_fwd(const hifa4_problem* p, const hifa4_fwd_options* opt, const void* q,
+                              const void* k_codes, const void* k_meta, const void* v_codes, const void* v_meta,
+                              const float* s, void* o, float* lse, void* workspace, size_t workspace_bytes,
+                              void* stream) {
+  Dims d;
+  hifa4_status st = check_problem(p, &d);
+  if (st != HIFA4_OK) return st;
+  if (!opt) return fail(HIFA4_ERR_INVALID_ARGUMENT, "options is NULL");
+  if (opt->norm != HIFA4_NORM_PREORDER && opt->norm != HIFA4_NORM_INCONSISTENT)
+    return fail(HIFA4_ERR_INVALID_ARGUMENT, "unknown norm %d", opt->norm);
+  if (opt->operands != HIFA4_OPERANDS_HIF4)
+    return fail(HIFA4_ERR_UNSUPPORTED, "decode reads a HIF4 cache: operands must be HIFA4_OPERANDS_HIF4");
+  if (opt->q_mean) return fail(HIFA4_ERR_UNSUPPORTED, "q_mean is not supported by decode (the cache has no key sums)");
+  if (p->num_heads_q / p->num_heads_kv > 8)
+    return fail(HIFA4_ERR_UNSUPPORTED, "decode supports at most 8 query heads per kv head (got %d)",
+                p->num_heads_q / p->num_heads_kv);
+  if (!q || !k_codes || !k_meta || !v_codes || !v_meta || !o || !lse)
+    return fail(HIFA4_ERR_INVALID_ARGUMENT, "null tensor pointer");
+  if ((opt->debug_p_codes == nullptr) != (opt->debug_p_meta == nullptr))
+    return fail(HIFA4_ERR_INVALID_ARGUMENT, "debug_p_codes and debug_p_meta must both be set or both be NULL");
+  if (opt->smooth_qk && !s) return fail(HIFA4_ERR_INVALID_ARGUMENT, "smooth_qk set but s is NULL");
+  if (d.tokens == 0 || d.S == 0) return HIFA4_OK;
+  const size_t need = hifa4_decode_workspace_bytes(p);
+  if (!workspace || workspace_bytes < need)
+    return fail(HIFA4_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu required", workspace_bytes, need);
+  hipStream_t hs = (hipStream_t)stream;
+  hipEvent_t* ev = (hipEvent_t*)opt->timing_events;
+  hipError_t e = hipSuccess;
+  if (ev && (e = hipEventRecord(ev[0], hs)) != hipSuccess) return hip_fail(e, "timing event");
+  hifa4::DecodeLaunch dl;
+  dl.q = (const hifa4::half_t*)q;
+  dl.s = opt->smooth_qk ? s : nullptr;
+  dl.cu = p->cu_seqlens;
+  dl.kc = (const uint8_t*)k_codes;
+  dl.km = (const uint32_t*)k_meta;
+  dl.vc = (const uint8_t*)v_codes;
+  dl.vm = (const uint32_t*)v_meta;
+  dl.o = (hifa4::half_t*)o;
+  dl.lse = lse;
+  dl.dbg_codes = (uint8_t*)opt->debug_p_codes;
+  dl.dbg_meta = (uint32_t*)opt->debug_p_meta;
+  dl.ws = (uint8_t*)workspace;
+  dl.ev = ev;
+  dl.batch = p->batch;
+  dl.S = d.S;
+  dl.NB = d.NB;
+  dl.hq = p->num_heads_q;
+  dl.hkv = p->num_heads_kv;
+  dl.D = p->head_dim;
+  dl.norm = opt->norm;
+  dl.c = (float)(1.4426950408889634 / std::sqrt((double)p->head_dim));
+  e = hifa4::launch_decode(dl, hs);
+  if (e != hipSuccess) return hip_fail(e, "decode kernels");
   if (ev && (e = hipEventRecord(ev[2], hs)) != hipSuccess) return hip_fail(e, "timing event");
   return HIFA4_OK;
 }

@@ -68,6 +68,16 @@ class Workload:
         (diagonal included), 2 flops per multiply-add, per query head."""
         return 4.0 * self.head_dim * self.heads_q * self.causal_pairs()
 
+    def decode_cache_bytes(self) -> int:
+        """Bytes of the packed HIF4 cache one decode step reads: K^ as 36 B
+        per 64 channels of every cached token and kv head, V^ as 36 B per
+        64-token group of every (block, kv head, channel)."""
+        s = self.seqlens().astype(np.int64)
+        g = self.head_dim // 64
+        k = int(s.sum()) * self.heads_kv * g * 36
+        v = int(((s + 63) // 64).sum()) * self.heads_kv * self.head_dim * 36
+        return k + v
+
     def outlier_channels(self) -> np.ndarray:
         """[Hkv, n] sorted channel indices that carry the K outlier."""
         if self.outliers_per_head == 0 and not self.outlier_fixed:
@@ -91,6 +101,10 @@ WORKLOADS = {
                             alpha=0.5, calib_from="qwen3_8b_s4096"),
     "varlen_b16": Workload("varlen_b16", 16, 32, 8, 128, 0, eval_seed=1,
                            varlen_lengths_seed=0, varlen_range=(512, 2048), alpha=0.0),
+    # one decode step per sequence over a 32768-token packed cache
+    "decode_b8_l32768": Workload("decode_b8_l32768", 8, 32, 8, 128, 32768, eval_seed=5,
+                                 outlier_seed=4242, outliers_per_head=4, outlier_scale=16.0,
+                                 alpha=0.5, calib_from="qwen3_8b_s4096"),
     "wide_d256": Workload("wide_d256", 2, 16, 8, 256, 8192, eval_seed=0,
                           calib_seeds=tuple(range(1001, 1017)), outlier_seed=4243,
                           outliers_per_head=8, outlier_scale=4.0, alpha=0.5, calib_seqlen=8192),
@@ -123,6 +137,26 @@ def make_inputs(w: Workload, seed: Optional[int] = None, seqlen: Optional[int] =
     s = w.seqlen if seqlen is None else seqlen
     q, k, v = _draw(rng, (b, s, w.heads_q, w.head_dim), (b, s, w.heads_kv, w.head_dim), w)
     return q, k, v, None
+
+
+def make_decode_inputs(w: Workload, seed: Optional[int] = None):
+    """A decode step: (q [B, Hq, D], k, v, cu_seqlens or None), fp16 numpy.
+    q is the query of each sequence's newest token; k and v are the cached
+    sequences ([B, S, Hkv, D], or [total, Hkv, D] with cu_seqlens when
+    varlen), the newest token included.  One generator draws q, then K, then V."""
+    rng = np.random.default_rng(w.eval_seed if seed is None else seed)
+    q = rng.standard_normal((w.batch, w.heads_q, w.head_dim), dtype=np.float32)
+    if w.q_bias:
+        q += np.float32(w.q_bias)
+    shape = (w.total_tokens(),) if w.varlen else (w.batch, w.seqlen)
+    k = rng.standard_normal(shape + (w.heads_kv, w.head_dim), dtype=np.float32)
+    v = rng.standard_normal(shape + (w.heads_kv, w.head_dim), dtype=np.float32)
+    ch = w.outlier_channels()
+    for h in range(w.heads_kv):
+        for c in ch[h]:
+            k[..., h, c] *= np.float32(w.outlier_scale)
+    return (q.astype(np.float16), k.astype(np.float16), v.astype(np.float16),
+            w.cu_seqlens() if w.varlen else None)
 
 
 def make_calibration(w: Workload, n: Optional[int] = None, seqlen: Optional[int] = None):

@@ -76,3 +76,34 @@ def test_workspace_sizes(lib):
     o16 = h.FwdOptions(0, 1, 0, None, None, None)
     assert lib.hifa4_workspace_bytes(ctypes.byref(p), ctypes.byref(o16)) == 64 * 8 * 32768
     assert lib.hifa4_workspace_bytes(ctypes.byref(_p(head_dim=80)), ctypes.byref(o)) == 0
+
+
+def _dec(lib, p, opt=None, ptr=1, ws=1 << 30):
+    opt = opt or h.FwdOptions(0, 0, 0, None, None, None)
+    return lib.hifa4_decode_fwd(ctypes.byref(p), ctypes.byref(opt), ptr, ptr, ptr, ptr, ptr, None, ptr, ptr,
+                                ptr, ws, None)
+
+
+def test_decode_validation_codes(lib):
+    assert _dec(lib, _p(head_dim=96)) == -2
+    assert _dec(lib, _p(), opt=h.FwdOptions(0, 1, 0, None, None, None)) == -2     # fp16 operands
+    assert "HIF4" in h.hifa4_last_error()
+    assert _dec(lib, _p(), opt=h.FwdOptions(0, 0, 0, None, None, None, 1)) == -2  # Q-Mean
+    assert "q_mean" in h.hifa4_last_error()
+    assert _dec(lib, _p(num_heads_q=32, num_heads_kv=2)) == -2                   # GQA group of 16
+    assert _dec(lib, _p(), ptr=None) == -1
+    assert _dec(lib, _p(), opt=h.FwdOptions(0, 0, 1, None, None, None)) == -1     # smooth without s
+    assert _dec(lib, _p(), opt=h.FwdOptions(0, 0, 0, None, 1, None)) == -1        # half a debug dump
+    assert _dec(lib, _p(), opt=h.FwdOptions(3, 0, 0, None, None, None)) == -1
+    assert _dec(lib, _p(), ws=16) == -3
+
+
+def test_decode_workspace_sizes(lib):
+    # B=2, Hq=32, D=128, S=4096: Q^ 2*32*2*32 B + meta 2*32*2*4 B (each
+    # rounded to 256 B), scores 2*32*64*64*2 B, block maxima 2*32*64*2 B,
+    # 8 splits of partial O (128 fp32) and l per row
+    p = _p(batch=2, max_seqlen=4096, num_heads_q=32, num_heads_kv=8)
+    rows = 2 * 32
+    want = 4096 + 512 + rows * 64 * 64 * 2 + rows * 64 * 2 + rows * 8 * 128 * 4 + rows * 8 * 4
+    assert lib.hifa4_decode_workspace_bytes(ctypes.byref(p)) == want
+    assert lib.hifa4_decode_workspace_bytes(ctypes.byref(_p(head_dim=80))) == 0

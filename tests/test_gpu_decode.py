@@ -1,0 +1,187 @@
+"""GPU parity of the decode step over a packed HIF4 cache.
+
+The oracle needs no decode mode: a decode step is row L-1 of the causal
+prefill of the cached sequence (the newest token sees every key).  For each
+sampled (sequence, kv head) the oracle runs that single row on the
+sequence's K and V with a query array whose last row is the decode query.
+Bit-exact: every P^ group of the decode kernels' debug dump; tolerance
+(|gpu - ref| <= 2e-3 + 1e-2*|ref|): O; LSE within 2e-3."""
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import attention as oatt
+from oracle import smooth as osmooth
+from paper_2607_04302_amd.workloads import WORKLOADS, make_calibration, make_decode_inputs, small_case
+
+from _gpu_util import check_close, to_gpu, to_np
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def h():
+    import paper_2607_04302_amd as mod
+    mod.load_library()
+    return mod
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _build_cache(h, k, v, s, cu, max_seqlen):
+    cu_t = None if cu is None else to_gpu(cu)
+    _, _, kc, km = h.hifa4_quantize_qk(None, to_gpu(k), None if s is None else to_gpu(s),
+                                       cu_seqlens=cu_t, max_seqlen=max_seqlen)
+    vc, vm = h.hifa4_quantize_v(to_gpu(v), cu_seqlens=cu_t, max_seqlen=max_seqlen)
+    return kc, km, vc, vm, cu_t
+
+
+def _oracle_row(qd_b, k_seq, v_seq, s, hk, grp, norm):
+    """Oracle of row L-1 for the grp query heads of kv head hk: returns the
+    result dicts of those heads (keys 0..grp-1)."""
+    L, d = k_seq.shape[0], k_seq.shape[2]
+    qs = np.zeros((1, L, grp, d), np.float16)
+    qs[0, L - 1] = qd_b[hk * grp:(hk + 1) * grp]
+    ks = k_seq[None, :, hk:hk + 1]
+    vs = v_seq[None, :, hk:hk + 1]
+    ss = None if s is None else s[hk:hk + 1]
+    ref = oatt.attention_fwd(qs, ks, vs, ss, norm=norm, rows=[L - 1], want_p=True)
+    return [ref[(0, j)] for j in range(grp)]
+
+
+def _decode_and_compare(h, qd, k, v, cu, s, max_seqlen, norm="preorder", seqs=None, kv_heads=None):
+    b_all = qd.shape[0]
+    hq, hkv = qd.shape[1], k.shape[-2]
+    grp = hq // hkv
+    kc, km, vc, vm, cu_t = _build_cache(h, k, v, s, cu, max_seqlen)
+    nm = h.NORM_PREORDER if norm == "preorder" else h.NORM_INCONSISTENT
+    o, lse, pc, pm = h.hifa4_decode_fwd(to_gpu(qd), kc, km, vc, vm, None if s is None else to_gpu(s),
+                                        cu_seqlens=cu_t, max_seqlen=max_seqlen, norm=nm, debug_p=True)
+    o, lse, pc, pm = to_np(o), to_np(lse), to_np(pc), to_np(pm).view(np.uint32)
+    worst = 0.0
+    for b in (range(b_all) if seqs is None else seqs):
+        if cu is None:
+            k_seq, v_seq = k[b], v[b]
+        else:
+            k_seq, v_seq = k[cu[b]:cu[b + 1]], v[cu[b]:cu[b + 1]]
+        L = k_seq.shape[0]
+        nb = -(-L // 64)
+        for hk in (range(hkv) if kv_heads is None else kv_heads):
+            for j, r in enumerate(_oracle_row(qd[b], k_seq, v_seq, s, hk, grp, norm)):
+                hh = hk * grp + j
+                worst = max(worst, check_close(o[b, hh], r["o"][0], what=f"O seq {b} head {hh}"))
+                check_close(lse[hh, b], r["lse"][0], atol=2e-3, rtol=0, what=f"LSE seq {b} head {hh}")
+                assert np.array_equal(pc[hh, b, :nb], r["p_codes"][0, :nb]), (b, hh)
+                assert np.array_equal(pm[hh, b, :nb], r["p_meta"][0, :nb]), (b, hh)
+    return worst
+
+
+def _last_queries(q, cu):
+    return np.stack([q[cu[b + 1] - 1] for b in range(len(cu) - 1)])
+
+
+@pytest.mark.parametrize("d,hq,hkv,lens,seed,smooth", [
+    (128, 4, 1, (300, 65, 64, 1, 190), 1, True),     # GQA x4, ragged tails, single token
+    (64, 2, 2, (129, 511), 2, False),                 # no GQA, D=64
+    (256, 8, 1, (200, 33), 3, True),                  # GQA x8 (two rows per wave), D=256
+    (128, 6, 2, (150, 700), 4, True),                 # GQA x3 (one wave idle)
+])
+def test_decode_varlen_parity(h, d, hq, hkv, lens, seed, smooth):
+    q, k, v, cu = small_case(heads_q=hq, heads_kv=hkv, head_dim=d, seqlens=lens, seed=seed)
+    s = np.exp(np.random.default_rng(seed).uniform(-1, 1, (hkv, d))).astype(np.float32) if smooth else None
+    qd = _last_queries(q, cu)
+    for norm in ("preorder", "inconsistent"):
+        _say("decode varlen", d, hq, hkv, lens, norm)
+        _decode_and_compare(h, qd, k, v, cu, s, max(lens), norm=norm)
+
+
+def test_decode_fixed_length(h):
+    """BSHD cache (every sequence max_seqlen tokens), three sequences."""
+    q, k, v, cu = small_case(heads_q=4, heads_kv=2, head_dim=128, seqlens=(130, 130, 130), seed=9)
+    qd = _last_queries(q, cu)
+    k4 = k.reshape(3, 130, 2, 128)
+    v4 = v.reshape(3, 130, 2, 128)
+    _say("decode fixed length")
+    _decode_and_compare(h, qd, k4, v4, None, None, 130)
+
+
+@pytest.mark.parametrize("length,d,hq,seed", [(5000, 128, 4, 5), (33000, 64, 2, 6)])
+def test_decode_many_splits(h, length, d, hq, seed):
+    """Long single sequences: 79 blocks in 10 splits, and 516 blocks in 65
+    splits (more than one 64-split pass of the merge)."""
+    q, k, v, cu = small_case(heads_q=hq, heads_kv=1, head_dim=d, seqlens=(length,), seed=seed)
+    s = np.exp(np.random.default_rng(seed).uniform(-1, 1, (1, d))).astype(np.float32)
+    _say("decode long", length)
+    _decode_and_compare(h, _last_queries(q, cu), k, v, cu, s, length)
+
+
+def test_decode_cache_append(h):
+    """The cache grows one token at a time: the K^ row of a new token
+    quantized alone, and the V^ block holding it re-quantized from that
+    block's fp16 tokens, equal the full-sequence quantization bit for bit;
+    each step's decode matches the oracle."""
+    import torch
+    d, hq, hkv = 128, 4, 2
+    q, k, v, cu = small_case(heads_q=hq, heads_kv=hkv, head_dim=d, seqlens=(131,), seed=11)
+    s = np.exp(np.random.default_rng(11).uniform(-1, 1, (hkv, d))).astype(np.float32)
+    s_t = to_gpu(s)
+    cap = 192
+    kc = torch.zeros((cap, hkv, d // 64, 32), dtype=torch.uint8, device="cuda")
+    km = torch.zeros((cap, hkv, d // 64), dtype=torch.int32, device="cuda")
+    vc = torch.zeros((1, cap // 64, hkv, d, 32), dtype=torch.uint8, device="cuda")
+    vm = torch.zeros((1, cap // 64, hkv, d), dtype=torch.int32, device="cuda")
+    k_t, v_t = to_gpu(k), to_gpu(v)
+    for L in range(120, 132):
+        if L == 120:
+            _, _, kc0, km0 = h.hifa4_quantize_qk(None, k_t[:L].contiguous(), s_t,
+                                                 cu_seqlens=to_gpu(np.array([0, L], np.int32)), max_seqlen=L)
+            kc[:L], km[:L] = kc0, km0
+        else:
+            _, _, kc1, km1 = h.hifa4_quantize_qk(None, k_t[L - 1:L].contiguous(), s_t,
+                                                 cu_seqlens=to_gpu(np.array([0, 1], np.int32)), max_seqlen=1)
+            kc[L - 1], km[L - 1] = kc1[0], km1[0]
+        j0 = (L - 1) // 64 * 64
+        blocks = range(L // 64 + 1) if L == 120 else [j0 // 64]
+        for J in blocks:
+            t1 = min(L, 64 * J + 64)
+            if t1 <= 64 * J:
+                continue
+            vb, vbm = h.hifa4_quantize_v(v_t[64 * J:t1].contiguous(),
+                                         cu_seqlens=to_gpu(np.array([0, t1 - 64 * J], np.int32)),
+                                         max_seqlen=t1 - 64 * J)
+            vc[0, J], vm[0, J] = vb[0, 0], vbm[0, 0]
+        nb = -(-L // 64)
+        full = _build_cache(h, k[:L], v[:L], s, np.array([0, L], np.int32), L)
+        assert torch.equal(kc[:L], full[0]) and torch.equal(km[:L], full[1])
+        assert torch.equal(vc[:, :nb], full[2]) and torch.equal(vm[:, :nb], full[3])
+        qd = q[L - 1][None]
+        cu_t = to_gpu(np.array([0, L], np.int32))
+        o, lse, pc, pm = h.hifa4_decode_fwd(to_gpu(qd), kc[:L], km[:L], vc[:, :nb].contiguous(),
+                                            vm[:, :nb].contiguous(), s_t, cu_seqlens=cu_t, max_seqlen=L,
+                                            debug_p=True)
+        o, lse, pc, pm = to_np(o), to_np(lse), to_np(pc), to_np(pm).view(np.uint32)
+        for hk in range(hkv):
+            for j, r in enumerate(_oracle_row(qd[0], k[:L], v[:L], s, hk, hq // hkv, "preorder")):
+                hh = hk * (hq // hkv) + j
+                check_close(o[0, hh], r["o"][0], what=f"O step {L} head {hh}")
+                check_close(lse[hh, 0], r["lse"][0], atol=2e-3, rtol=0, what="LSE")
+                assert np.array_equal(pc[hh, 0, :nb], r["p_codes"][0, :nb]), (L, hh)
+                assert np.array_equal(pm[hh, 0, :nb], r["p_meta"][0, :nb]), (L, hh)
+    _say("decode append ok")
+
+
+def test_decode_b8_l32768_sampled(h):
+    """The decode workload at full size in the benchmark's launch shape (8
+    sequences of 32768 cached tokens, Qwen3-8B heads, Smooth-QK scales from
+    the Qwen3-shaped calibration draw): sampled sequences and kv heads, every
+    P^ code of those rows bit-exact, O and LSE."""
+    w = WORKLOADS["decode_b8_l32768"]
+    qd, k, v, _ = make_decode_inputs(w)
+    qc, kc = make_calibration(WORKLOADS[w.calib_from], n=4)
+    s, _ = osmooth.calibrate(qc, kc, w.heads_kv, w.alpha)
+    _say("decode_b8_l32768 sampled")
+    _decode_and_compare(h, qd, k, v, None, s, w.seqlen, seqs=[0, 7], kv_heads=[0, 5])
