@@ -143,6 +143,63 @@ def config_report(h, torch, np, name, ws):
     return out
 
 
+def decode_report(h, torch, np, ws, steps=50):
+    """One decode step per sequence over the packed HIF4 cache of the
+    8 x 32768-token decode workload (Qwen3-8B heads, Smooth-QK scales from
+    the Qwen3-shaped calibration draw): the cache is built once on the GPU,
+    then back-to-back decode calls are timed with HIP events recorded by the
+    library (before the query quantization, after the score kernel, after the
+    merge).  HBM roofline on the bytes of the packed cache a step reads."""
+    from paper_2607_04302_amd.workloads import WORKLOADS, make_calibration, make_decode_inputs
+    w = WORKLOADS["decode_b8_l32768"]
+    dev = torch.device("cuda:0")
+    qn, kn, vn, _ = make_decode_inputs(w)
+    qc, kc = make_calibration(WORKLOADS[w.calib_from])
+    s, _ = h.hifa4_calibrate_smooth_qk(torch.from_numpy(qc).to(dev), torch.from_numpy(kc).to(dev), w.alpha)
+    del qc, kc
+    q = torch.from_numpy(qn).to(dev)
+    k = torch.from_numpy(kn).to(dev)
+    v = torch.from_numpy(vn).to(dev)
+    _, _, kcode, kmeta = h.hifa4_quantize_qk(None, k, s)
+    vcode, vmeta = h.hifa4_quantize_v(v)
+    del k, v
+    torch.cuda.empty_cache()
+    out = torch.empty_like(q)
+    lse = torch.empty((w.heads_q, w.batch), dtype=torch.float32, device=dev)
+    kw = dict(out=out, lse=lse, workspace=ws)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    for trio in evs:
+        for e in trio:
+            e.record()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < 0.2:
+        for _ in range(10):
+            h.hifa4_decode_fwd(q, kcode, kmeta, vcode, vmeta, s, **kw)
+        torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        h.hifa4_decode_fwd(q, kcode, kmeta, vcode, vmeta, s, timing_events=evs[i], **kw)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) * 1e3 / steps
+    first = sum(evs[i][0].elapsed_time(evs[i][1]) for i in range(steps)) / steps
+    second = sum(evs[i][1].elapsed_time(evs[i][2]) for i in range(steps)) / steps
+    cache = w.decode_cache_bytes()
+    dev_ms = first + second
+    gbs = cache / (dev_ms * 1e-3) / 1e9
+    res = {"workload": w.name, "batch": w.batch, "heads_q": w.heads_q, "heads_kv": w.heads_kv,
+           "head_dim": w.head_dim, "cached_tokens_per_sequence": w.seqlen, "smooth_qk": True,
+           "cache_bytes": cache, "fp16_cache_bytes": 2 * 2 * w.total_tokens() * w.heads_kv * w.head_dim,
+           "steps": steps, "ms_per_step": round(wall, 4),
+           "kernels_ms": {"q_quant_and_scores": round(first, 4), "splits_and_merge": round(second, 4)},
+           "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                        "frac": round(gbs / PEAK_HBM_GBS, 4),
+                        "basis": "packed K^ and V^ cache bytes per step / device time of the step"}}
+    del q, kcode, kmeta, vcode, vmeta, out, lse
+    torch.cuda.empty_cache()
+    return res
+
+
 def p_only_study(h, torch, np, args, q, k, v, out16, ws):
     """The P-only local operator (Q, K, V fp16, only P quantized) on the same
     inputs, with the consistent (P-Reordering) and the inconsistent
@@ -234,6 +291,9 @@ def main():
     ap.add_argument("--cpu-heads", type=int, default=16)
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the throughput of the other workloads (tiny, long, varlen, wide)")
+    ap.add_argument("--no-decode", action="store_true", help="skip the decode step over the packed cache")
+    ap.add_argument("--decode-only", action="store_true",
+                    help="only time the decode step (for profiling its kernels) and print its report")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB five times (the reference kernel that "
                          "scales HBM traffic counters) and exit")
@@ -263,6 +323,9 @@ def main():
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
+    if args.decode_only:
+        print(json.dumps({"decode": decode_report(h, torch, np, h.Workspace(), steps=args.steps)}), flush=True)
+        return
     w = WORKLOADS[args.workload]
     if w.varlen:
         print("bench.py times fixed-length workloads", file=sys.stderr)
@@ -354,6 +417,8 @@ def main():
         torch.cuda.empty_cache()
         result["other_configs"] = [config_report(h, torch, np, name, ws)
                                    for name in ("tiny_s256", "long_s32768", "varlen_b16", "wide_d256")]
+    if not args.no_decode:
+        result["decode"] = decode_report(h, torch, np, ws)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, qn, kn, vn, sn, args.cpu_heads)
     print(json.dumps(result), flush=True)

@@ -189,8 +189,8 @@ hifa4_status hifa4_decode_fwd(const hifa4_problem* p, const hifa4_fwd_options* o
   if (opt->operands != HIFA4_OPERANDS_HIF4)
     return fail(HIFA4_ERR_UNSUPPORTED, "decode reads a HIF4 cache: operands must be HIFA4_OPERANDS_HIF4");
   if (opt->q_mean) return fail(HIFA4_ERR_UNSUPPORTED, "q_mean is not supported by decode (the cache has no key sums)");
-  if (p->num_heads_q / p->num_heads_kv > 8)
-    return fail(HIFA4_ERR_UNSUPPORTED, "decode supports at most 8 query heads per kv head (got %d)",
+  if (p->num_heads_q / p->num_heads_kv > 16)
+    return fail(HIFA4_ERR_UNSUPPORTED, "decode supports at most 16 query heads per kv head (got %d)",
                 p->num_heads_q / p->num_heads_kv);
   if (!q || !k_codes || !k_meta || !v_codes || !v_meta || !o || !lse)
     return fail(HIFA4_ERR_INVALID_ARGUMENT, "null tensor pointer");

@@ -11,21 +11,38 @@
 // range is split; the split must not change any P^ code, because P^ depends
 // on the running maximum entering each 64-key block.  Three kernels keep every
 // decision of the sequential loop:
-//   1. scores: per (sequence, kv head, 64-key block) the fp16 scores S2 of the
-//      GQA group's query rows, stored, and each row's block maximum;
-//   2. splits: each workgroup takes a run of blocks and starts from the
-//      running maximum the sequential loop has at its first block (the prefix
-//      maximum of the stored block maxima), then applies the FP16 softmax,
+//   1. scores: per (sequence, run of 64-key blocks, kv head) the fp16 scores
+//      S2 of the GQA group's query rows, stored, and each row's block maximum;
+//   2. splits: each wave takes a run of blocks and starts from the running
+//      maximum the sequential loop has at its first block (the prefix maximum
+//      of the stored block maxima), then applies the FP16 softmax,
 //      P^ = HIF4(P) and the PV product as the sequential loop does; it writes
 //      its partial O_s and l_s, both relative to the running maximum at its
 //      last block;
 //   3. merge: O = sum_s O_s R_s and l = sum_s l_s R_s, where R_s is the product
 //      of the rescale factors r_J = E(fp16(m_{J-1} - m_J)) of all blocks after
 //      split s: the sequential recurrence O <- r_J O + P^_J V^_J unrolled.
-// Cache values are decoded to exact fp32 values in LDS: an element is
-// +-u 2^-sh b/4 (u <= 7, sh <= 2, b with three significant bits), and every
-// product and partial sum of a 64-element group dot of such values is exact in
-// fp32, so the scores follow the library's score contract bit for bit.
+//
+// Both contractions run on the int8 MFMA (32x32x32, int32 accumulate).  A HIF4
+// element is +-u 2^-sh times b/4 (u <= 7, sh <= 2), so 4 u 2^-sh = +-u << (2-sh)
+// is an integer in [-28, 28]: the group's codes become int8 operands with two
+// shifts and a sign fix per four elements, every 64-element dot product is
+// exact in int32, and the bases (E6M2, three significant bits) are applied
+// in an fp32 epilogue where every product stays exact.  The scores therefore
+// follow the library's score contract bit for bit, and the PV partial sums of
+// a block are exact before the fp32 rescale-and-add.
+//
+// MFMA operand convention: lane l holds row / column (l & 31) of A / B and
+// sixteen k indices chosen by the half h = l >> 5; a 64-element group is two
+// MFMAs, the first over the group's quarters 2h (bytes 16h..16h+7), the
+// second over quarters 2h+1 (bytes 16h+8..16h+15), so each lane reads 16
+// contiguous code bytes.  Only the pairing of k indices between A and B
+// matters for a dot product, and both operands place a quarter's sixteen
+// elements in the same (decode) order.  The output lane l holds column
+// (l & 31) and, in its first four values, rows 4h + c.
+//
+// Workgroups hold one wave per kv head (up to eight): the heads of a token
+// share cache lines, so the lines are read once by one compute unit.
 #include "hifa4_device.h"
 #include "hifa4_internal.h"
 
@@ -33,46 +50,70 @@ namespace hifa4 {
 
 namespace {
 
-constexpr int kBlocksPerSplit = 8;
-constexpr int kMaxRowsPerWave = 2;   // GQA groups up to 8 query heads per kv head
-constexpr int kMaxChPerLane = 4;     // head_dim up to 256
+typedef int i4_t __attribute__((ext_vector_type(4)));
+typedef int i16_t __attribute__((ext_vector_type(16)));
+typedef unsigned short u16x2_t __attribute__((ext_vector_type(2)));
+
+constexpr int kScoreBlocksPerWave = 8;
+constexpr int kBlocksPerSplit = 8;       // a power of two <= 64
+constexpr int kMaxWaves = 8;             // kv heads per workgroup
 
 __device__ __forceinline__ int dseq_start(const int* cu, int b, int S) { return cu ? cu[b] : b * S; }
 __device__ __forceinline__ int dseq_len(const int* cu, int b, int S) { return cu ? cu[b + 1] - cu[b] : S; }
 
-// Sixteen consecutive elements e0..e0+15 of a canonical group, as exact fp32
-// values +-u * 2^-sh * scale (scale = b/4 for the dequantized value, 1 for the
-// operand value u * 2^-sh).  w holds the group's code bytes e0/2 .. e0/2+7.
-__device__ __forceinline__ void decode16(uint2 w, uint32_t meta, int e0, float scale, float out[16]) {
-#pragma unroll
-  for (int e = 0; e < 16; ++e) {
-    const uint32_t word = e < 8 ? w.x : w.y;
-    const uint32_t nib = (word >> (4 * (e & 7))) & 15u;
-    const int ea = e0 + e;
-    const int sh = (int)((meta >> (8 + (ea >> 3))) & 1u) + (int)((meta >> (16 + (ea >> 2))) & 1u);
-    const float step = scale * (sh == 0 ? 1.0f : (sh == 1 ? 0.5f : 0.25f));
-    const float v = (float)(nib & 7u) * step;
-    out[e] = (nib & 8u) ? -v : v;
-  }
-}
-
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-  return v;
-}
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
-  return v;
-}
-// maximum over aligned groups of `width` lanes (width a power of two <= 64)
-__device__ __forceinline__ float group_max(float v, int width) {
-  for (int o = width >> 1; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-  return v;
-}
 __device__ __forceinline__ half_t exp2_h(half_t x) { return exp2_h2(h2_t{x, (half_t)0})[0]; }
 __device__ __forceinline__ half_t hmax(half_t a, half_t b) { return a > b ? a : b; }
+
+// Shift amounts 2 - sh of the two E3 blocks of each of the words 2Q and 2Q+1
+// of a group (elements 16Q..16Q+15), packed as 16-bit halves: low half =
+// first four elements of the word, high half = last four.
+__device__ __forceinline__ void quarter_shifts(uint32_t meta, int Q, uint32_t& k0, uint32_t& k1) {
+  const uint32_t e2 = (meta >> (8 + 2 * Q)) & 3u;        // E2 of words 2Q, 2Q+1
+  const uint32_t e3 = (meta >> (16 + 4 * Q)) & 15u;      // E3 of blocks 4Q..4Q+3
+  const uint32_t a0 = e2 & 1u, a1 = e2 >> 1;
+  k0 = (2u - a0 - (e3 & 1u)) | ((2u - a0 - ((e3 >> 1) & 1u)) << 16);
+  k1 = (2u - a1 - ((e3 >> 2) & 1u)) | ((2u - a1 - (e3 >> 3)) << 16);
+}
+
+// Four sign-magnitude elements, one per byte (magnitude in `mag`, sign bit in
+// bit 0 of each byte of `sgn`), to int8 +-mag << k with k per 16-bit half.
+// The magnitudes stay below 32 after the shift, so no byte spills into the
+// next; a zero magnitude never carries a sign (zero is stored as +0).
+__device__ __forceinline__ uint32_t to_i8x4(uint32_t mag, uint32_t sgn, uint32_t k) {
+  const u16x2_t v = __builtin_bit_cast(u16x2_t, mag) << __builtin_bit_cast(u16x2_t, k);
+  const uint32_t m = __builtin_bit_cast(uint32_t, v);
+  const uint32_t neg = (sgn << 8) - sgn;                 // 0xff in every negative byte
+  return (m ^ neg) + sgn;                                // per-byte two's complement
+}
+
+// Sixteen elements (the 8 code bytes w of quarter Q of a group) as int8
+// operands 4 * (+-u 2^-sh).  Byte order: register 0 = elements 0,2,4,6,
+// register 1 = 1,3,5,7, register 2 = 8,10,12,14, register 3 = 9,11,13,15
+// (relative to 16Q).
+__device__ __forceinline__ i4_t decode_quarter(uint32_t wx, uint32_t wy, uint32_t meta, int Q) {
+  uint32_t k0, k1;
+  quarter_shifts(meta, Q, k0, k1);
+  i4_t r;
+  r[0] = (int)to_i8x4(wx & 0x07070707u, (wx >> 3) & 0x01010101u, k0);
+  r[1] = (int)to_i8x4((wx >> 4) & 0x07070707u, (wx >> 7) & 0x01010101u, k0);
+  r[2] = (int)to_i8x4(wy & 0x07070707u, (wy >> 3) & 0x01010101u, k1);
+  r[3] = (int)to_i8x4((wy >> 4) & 0x07070707u, (wy >> 7) & 0x01010101u, k1);
+  return r;
+}
+
+// Byte index, inside the 16-byte operand of a quarter, of its element e
+// (0..15) in the order decode_quarter produces.
+__device__ __forceinline__ constexpr int operand_byte(int e) {
+  return 4 * (2 * (e >> 3) + (e & 1)) + ((e & 7) >> 1);
+}
+
+// Exact int32 dot products of a whole 64-element group: the MFMA over the
+// lane's first quarter, then the second, accumulated.
+__device__ __forceinline__ i16_t group_dot(i4_t a0, i4_t a1, uint4 w, uint32_t meta, int h) {
+  const i16_t z = {};
+  const i16_t c = __builtin_amdgcn_mfma_i32_32x32x32_i8(a0, decode_quarter(w.x, w.y, meta, 2 * h), z, 0, 0, 0);
+  return __builtin_amdgcn_mfma_i32_32x32x32_i8(a1, decode_quarter(w.z, w.w, meta, 2 * h + 1), c, 0, 0, 0);
+}
 
 struct DecodeArgs {
   const uint8_t* qc;       // canonical Q^ of the decode rows [batch, Hq, G, 32]
@@ -90,258 +131,424 @@ struct DecodeArgs {
   float* lse;              // [Hq, batch]
   uint8_t* dbg_codes;      // [Hq, batch, NB, 32] or null
   uint32_t* dbg_meta;      // [Hq, batch, NB]
-  int batch, S, NB, hq, hkv, D, n_split;
+  int batch, S, NB, hq, hkv, D, n_split, waves;
   float c;
 };
 
 // ---------------------------------------------------------------------------
-// 1. Scores and block maxima.  Workgroup (J, hk, b), 256 threads.  The query
-// rows of the GQA group are kept as operand values and group weights
-// w_g = fp32(b_g/4 * c); the block's K^ is decoded one 64-channel group at a
-// time into LDS as [channel][key]; wave w owns the rows w and w+4 with
-// lane = key, so each lane forms the exact group dot d_g and the accumulator
-// acc = fp32(d_0 w_0), then acc = fma(d_g, w_g, acc).
-__global__ void __launch_bounds__(256) k_decode_scores(DecodeArgs a) {
-  __shared__ float kt[64 * 64];
-  __shared__ float qw[8 * 4];
-  extern __shared__ float qo[];              // [grp][D]
-  const int J = blockIdx.x, hk = blockIdx.y, b = blockIdx.z;
+// 1. Scores and block maxima.  Wave = kv head, workgroup = (kv heads, run of
+// blocks, sequence).  A = the GQA group's query rows (rows >= the group size
+// are zero), B = 32 keys of the block; per (32-key tile, channel group) the
+// two MFMAs give the exact group dots 16 * sum(q_unit * k_unit) of query rows
+// 4h + c with key (l & 31) of the tile.  Epilogue per group: d_g = dot * b_K/64
+// (exact), acc = fp32(d_0 w_0), then acc = fma(d_g, w_g, acc) with
+// w_g = fp32(b_Q,g/4 * c); S2 = fp16(acc).  Two register buffers in fixed
+// roles keep the next two blocks' codes in flight; the scores and maxima of
+// the run are collected in LDS and stored after the last block, so the loop
+// issues loads only.
+template <int G>
+__global__ void __launch_bounds__(64 * kMaxWaves, (G <= 2 ? 4 : 2)) k_decode_scores(DecodeArgs a) {
+  __shared__ __align__(16) half_t lds_s[kMaxWaves][8][kScoreBlocksPerWave * 64];
+  __shared__ half_t lds_m[kMaxWaves][8][kScoreBlocksPerWave];
+  const int wave = (int)(threadIdx.x >> 6);
+  const int hk = blockIdx.x * a.waves + wave;
+  if (hk >= a.hkv) return;
+  const int lane = threadIdx.x & 63, n = lane & 31, h = lane >> 5;
+  const int b = blockIdx.z;
   const int L = dseq_len(a.cu, b, a.S);
-  if (64 * J >= L) return;
+  const int nblk = (L + 63) >> 6;
+  const int J0 = blockIdx.y * kScoreBlocksPerWave;
+  if (J0 >= nblk) return;
+  const int J1 = min(J0 + kScoreBlocksPerWave, nblk);
   const int t0 = dseq_start(a.cu, b, a.S);
-  const int D = a.D, G = D >> 6, grp = a.hq / a.hkv;
-  const int nk = min(64, L - 64 * J);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  for (int it = tid; it < grp * G * 4; it += 256) {
-    const int r = it / (4 * G), g = (it >> 2) % G, qt = it & 3;
-    const size_t qi = ((size_t)b * a.hq + hk * grp + r) * G + g;
-    const uint32_t meta = a.qm[qi];
-    const uint2 w = *reinterpret_cast<const uint2*>(a.qc + qi * 32 + 8 * qt);
-    float v[16];
-    decode16(w, meta, 16 * qt, 1.0f, v);
+  const int grp = a.hq / a.hkv;
+  const size_t row0 = (size_t)b * a.hq + (size_t)hk * grp;     // first query row of the group
+  struct KBlock {
+    uint4 w[2][G];
+    uint32_t meta[2][G];
+  };
+  auto load = [&](int J, KBlock& kb) {
 #pragma unroll
-    for (int e = 0; e < 16; ++e) qo[r * D + 64 * g + 16 * qt + e] = v[e];
-    if (qt == 0) qw[r * G + g] = (0.25f * e6m2_value(meta & 255u)) * a.c;
-  }
-  float acc[kMaxRowsPerWave] = {0.0f, 0.0f};
+    for (int t = 0; t < 2; ++t) {
+      const int key = 64 * J + 32 * t + n;
+      const int kk = key < L ? key : L - 1;                  // rows past the end are masked below
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const size_t gi = ((size_t)(t0 + kk) * a.hkv + hk) * G + g;
+        kb.w[t][g] = *reinterpret_cast<const uint4*>(a.kc + gi * 32 + 16 * h);
+        kb.meta[t][g] = a.km[gi];
+      }
+    }
+  };
+  // the query rows: codes of row n, weights of the output rows 4h + c
+  const int qr = n < grp ? n : 0;
+  uint4 qw4[G];
+  uint32_t qmeta[G];
+#pragma unroll
   for (int g = 0; g < G; ++g) {
-    __syncthreads();
-    {
-      const int key = lane, qt = wave;       // 64 keys x 4 quarters of 16 elements
-      float v[16];
-      if (key < nk) {
-        const size_t gi = ((size_t)(t0 + 64 * J + key) * a.hkv + hk) * G + g;
-        const uint32_t meta = a.km[gi];
-        const uint2 w = *reinterpret_cast<const uint2*>(a.kc + gi * 32 + 8 * qt);
-        decode16(w, meta, 16 * qt, 0.25f * e6m2_value(meta & 255u), v);
-      } else {
+    const size_t qi = (row0 + qr) * G + g;
+    qw4[g] = *reinterpret_cast<const uint4*>(a.qc + qi * 32 + 16 * h);
+    qmeta[g] = a.qm[qi];
+  }
+  // every prefetch is unconditional (past the run's end it reloads the last
+  // block), so the number of loads in flight is the same on every path
+  KBlock b0, b1;
+  load(J0, b0);
+  load(min(J0 + 1, J1 - 1), b1);
+  i4_t qa[G][2];
+  float wq[G][4];
 #pragma unroll
-        for (int e = 0; e < 16; ++e) v[e] = 0.0f;
+  for (int g = 0; g < G; ++g) {
+    qa[g][0] = qa[g][1] = i4_t{0, 0, 0, 0};
+    if (n < grp) {
+      qa[g][0] = decode_quarter(qw4[g].x, qw4[g].y, qmeta[g], 2 * h);
+      qa[g][1] = decode_quarter(qw4[g].z, qw4[g].w, qmeta[g], 2 * h + 1);
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const uint32_t mr = (uint32_t)__shfl((int)qmeta[g], 4 * h + c);
+      wq[g][c] = (0.25f * e6m2_value(mr & 255u)) * a.c;
+    }
+  }
+  half_t* ls = &lds_s[wave][0][0];
+  auto compute = [&](const KBlock& kb, int i) {
+    const int J = J0 + i;
+    float acc[2][4];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const uint32_t meta = kb.meta[t][g];
+        const i16_t dot = group_dot(qa[g][0], qa[g][1], kb.w[t][g], meta, h);
+        const float bk = e6m2_value(meta & 255u) * 0.015625f;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const float d = (float)dot[c] * bk;                      // exact
+          acc[t][c] = g == 0 ? d * wq[0][c] : __builtin_fmaf(d, wq[g][c], acc[t][c]);
+        }
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int r = 4 * h + c;
+      half_t sv[2];
+      float m = -__builtin_inff();
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        sv[t] = 64 * J + 32 * t + n < L ? (half_t)acc[t][c] : (half_t)(-__builtin_inff());
+        m = fmaxf(m, (float)sv[t]);
       }
 #pragma unroll
-      for (int e = 0; e < 16; ++e) kt[(16 * qt + e) * 64 + key] = v[e];
+      for (int o = 1; o < 32; o <<= 1) m = fmaxf(m, __shfl_xor(m, o));
+      if (r < grp) {
+        ls[r * (kScoreBlocksPerWave * 64) + 64 * i + n] = sv[0];
+        ls[r * (kScoreBlocksPerWave * 64) + 64 * i + 32 + n] = sv[1];
+        if (n == 0) lds_m[wave][r][i] = (half_t)m;
+      }
     }
-    __syncthreads();
+  };
 #pragma unroll
-    for (int i = 0; i < kMaxRowsPerWave; ++i) {
-      const int r = wave + 4 * i;
-      if (r >= grp) break;
-      const float* qr = qo + r * D + 64 * g;
-      float d = 0.0f;                          // exact: every partial sum fits fp32
-#pragma unroll 16
-      for (int ch = 0; ch < 64; ++ch) d = __builtin_fmaf(qr[ch], kt[ch * 64 + lane], d);
-      const float w = qw[r * G + g];
-      acc[i] = g == 0 ? d * w : __builtin_fmaf(d, w, acc[i]);
-    }
+  for (int i = 0; i < kScoreBlocksPerWave; i += 2) {
+    if (J0 + i < J1) compute(b0, i);
+    if (i + 2 < kScoreBlocksPerWave) load(min(J0 + i + 2, J1 - 1), b0);
+    if (J0 + i + 1 < J1) compute(b1, i + 1);
+    if (i + 3 < kScoreBlocksPerWave) load(min(J0 + i + 3, J1 - 1), b1);
   }
-#pragma unroll
-  for (int i = 0; i < kMaxRowsPerWave; ++i) {
-    const int r = wave + 4 * i;
-    if (r >= grp) break;
-    const half_t s2 = lane < nk ? (half_t)acc[i] : (half_t)(-__builtin_inff());
-    const size_t row = (size_t)b * a.hq + hk * grp + r;
-    a.s2[(row * a.NB + J) * 64 + lane] = s2;
-    const float m = wave_max((float)s2);
-    if (lane == 0) a.mx[row * a.NB + J] = (half_t)m;
+  // the run's scores (J1 - J0 blocks of 64, contiguous per row) and maxima
+  const int nb = J1 - J0;
+  for (int r = 0; r < grp; ++r) {
+    const uint2* src = reinterpret_cast<const uint2*>(ls + r * (kScoreBlocksPerWave * 64));
+    uint2* dst = reinterpret_cast<uint2*>(a.s2 + ((row0 + r) * a.NB + J0) * 64);
+    for (int k = lane; k < nb * 16; k += 64) dst[k] = src[k];
+    if (lane < nb) a.mx[(row0 + r) * a.NB + J0 + lane] = lds_m[wave][r][lane];
   }
 }
 
 // ---------------------------------------------------------------------------
-// 2. Splits.  Workgroup (split, hk, b), 256 threads: wave w owns the rows w
-// and w+4; lane = key for the softmax and P^, lane + 64j = channel for O.
-template <int NORM, bool DEBUG>
-__global__ void __launch_bounds__(256) k_decode_split(DecodeArgs a) {
-  extern __shared__ float dsm[];
-  const int sp = blockIdx.x, hk = blockIdx.y, b = blockIdx.z;
+// 2. Splits.  Wave = kv head, workgroup = (kv heads, split, sequence).  Per
+// block, the FP16 softmax and P^ = HIF4(P) run on every lane: lane i takes
+// query row 4p + (i >> 4) (pass p < RP) and its keys 4(i & 15)..+3, one E3
+// block; E2 pairs two lanes, the row base sixteen.  The int8 values
+// 4 u 2^-sh go to LDS in the A-operand layout (row, quarter, decode order),
+// from where lane (row l & 31, half h) reads its two operands.  B = 32
+// channels of the block's V^ groups; per 32-channel tile the two MFMAs give
+// the exact block sums, and O[row][ch] = fma(O, r_row, dot * b_V/16 * b_P/16).
+template <int NT, int RP, int NORM, bool DEBUG>
+__global__ void __launch_bounds__(64 * kMaxWaves, (NT <= 4 ? 4 : 2)) k_decode_split(DecodeArgs a) {
+  constexpr int D = 32 * NT;
+  __shared__ __align__(16) uint8_t lds_p[kMaxWaves][8 * 64];
+  const int wave = (int)(threadIdx.x >> 6);
+  const int hk = blockIdx.x * a.waves + wave;
+  if (hk >= a.hkv) return;
+  const int lane = threadIdx.x & 63, n = lane & 31, h = lane >> 5;
+  const int sp = blockIdx.y, b = blockIdx.z;
   const int L = dseq_len(a.cu, b, a.S);
   const int nblk = (L + 63) >> 6;
   const int J0 = sp * kBlocksPerSplit;
   if (J0 >= nblk) return;
   const int J1 = min(J0 + kBlocksPerSplit, nblk);
-  const int D = a.D, grp = a.hq / a.hkv;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  float* vv = dsm;                 // [64 keys][D]
-  float* ph = vv + 64 * D;         // [grp][64]
-  float O[kMaxRowsPerWave][kMaxChPerLane];
-  float l[kMaxRowsPerWave];
-  half_t m[kMaxRowsPerWave];
+  const int grp = a.hq / a.hkv;
+  const size_t row0 = (size_t)b * a.hq + (size_t)hk * grp;
+  uint8_t* lp = lds_p[wave];
+  const int kq = lane & 15;                      // keys 4kq..4kq+3 of the block
+  const int quarter = kq >> 2;                   // their group quarter
+  int prow[RP];                                  // softmax row of this lane per pass
 #pragma unroll
-  for (int i = 0; i < kMaxRowsPerWave; ++i) {
-    l[i] = 0.0f;
-#pragma unroll
-    for (int j = 0; j < kMaxChPerLane; ++j) O[i][j] = 0.0f;
-    const int r = wave + 4 * i;
-    float pm = -__builtin_inff();
-    if (r < grp) {
-      // the running maximum entering block J0: the prefix maximum
-      const size_t row = (size_t)b * a.hq + hk * grp + r;
-      for (int j = lane; j < J0; j += 64) pm = fmaxf(pm, (float)a.mx[row * a.NB + j]);
-      pm = wave_max(pm);
-    }
-    m[i] = (half_t)pm;
+  for (int p = 0; p < RP; ++p) {
+    const int r = 4 * p + (lane >> 4);
+    prow[p] = r < grp ? r : 0;
   }
-  for (int J = J0; J < J1; ++J) {
-    // V^ block: D groups of 64 tokens, decoded into [token][channel]
-    for (int it = tid; it < 4 * D; it += 256) {
-      const int ch = it % D, qt = it / D;
-      const size_t gi = (((size_t)b * a.NB + J) * a.hkv + hk) * D + ch;
-      const uint32_t meta = a.vm[gi];
-      const uint2 w = *reinterpret_cast<const uint2*>(a.vc + gi * 32 + 8 * qt);
-      float v[16];
-      decode16(w, meta, 16 * qt, 0.25f * e6m2_value(meta & 255u), v);
+  struct VBlock {
+    uint4 w[NT];
+    uint32_t meta[NT];
+    uint2 s[RP];
+    half_t mx[RP];
+  };
+  auto load = [&](int J, VBlock& vb) {
+    const size_t vg = (((size_t)b * a.NB + J) * a.hkv + hk) * D;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) vv[(16 * qt + e) * D + ch] = v[e];
+    for (int t = 0; t < NT; ++t) {
+      const size_t gi = vg + 32 * t + n;
+      vb.w[t] = *reinterpret_cast<const uint4*>(a.vc + gi * 32 + 16 * h);
+      vb.meta[t] = a.vm[gi];
     }
-    float rr[kMaxRowsPerWave];
 #pragma unroll
-    for (int i = 0; i < kMaxRowsPerWave; ++i) {
-      const int r = wave + 4 * i;
-      rr[i] = 1.0f;
-      if (r >= grp) break;
-      const size_t row = (size_t)b * a.hq + hk * grp + r;
-      const half_t s2 = a.s2[(row * a.NB + J) * 64 + lane];
-      const half_t mn = hmax(m[i], a.mx[row * a.NB + J]);
-      const half_t p16 = exp2_h(s2 - mn);     // fp16 difference, then E
-      rr[i] = (float)exp2_h(m[i] - mn);
-      m[i] = mn;
-      // P^ = HIF4(P) over the block's 64 keys (lane = key)
-      const float ap = (float)p16;
-      const uint32_t base = e6m2_ceil(wave_max(ap));
+    for (int p = 0; p < RP; ++p) {
+      const size_t rj = (row0 + prow[p]) * a.NB + J;
+      vb.s[p] = *reinterpret_cast<const uint2*>(a.s2 + rj * 64 + 4 * kq);
+      vb.mx[p] = a.mx[rj];
+    }
+  };
+  // every prefetch is unconditional (past the split's end it reloads the last
+  // block), so the number of loads in flight is the same on every path
+  VBlock b0, b1;
+  load(J0, b0);
+  load(min(J0 + 1, J1 - 1), b1);
+  // the running maximum entering block J0 of each softmax row: the prefix
+  // maximum of the block maxima, with every load of a row issued at once
+  half_t m[RP];
+  float l[RP];
+#pragma unroll
+  for (int p = 0; p < RP; ++p) {
+    m[p] = (half_t)(-__builtin_inff());
+    l[p] = 0.0f;
+  }
+  for (int r = 0; r < grp; ++r) {
+    float pm = -__builtin_inff();
+    for (int j0 = 0; j0 < J0; j0 += 64 * 8) {
+      half_t v[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int j = j0 + 64 * k + lane;
+        v[k] = a.mx[(row0 + r) * a.NB + (j < J0 ? j : 0)];
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        if (j0 + 64 * k + lane < J0) pm = fmaxf(pm, (float)v[k]);
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) pm = fmaxf(pm, __shfl_xor(pm, o));
+#pragma unroll
+    for (int p = 0; p < RP; ++p)
+      if (4 * p + (lane >> 4) == r) m[p] = (half_t)pm;
+  }
+  float O[NT][4];
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) O[t][c] = 0.0f;
+  auto block = [&](const VBlock& cur, int J) {
+    float rr[RP], sp16[RP];
+#pragma unroll
+    for (int p = 0; p < RP; ++p) {
+      const int r = 4 * p + (lane >> 4);
+      // FP16 softmax of the lane's four keys
+      const half_t mn = hmax(m[p], cur.mx[p]);
+      rr[p] = (float)exp2_h(m[p] - mn);
+      m[p] = mn;
+      const h2_t mn2 = {mn, mn};
+      const h2_t p01 = exp2_h2(__builtin_bit_cast(h2_t, cur.s[p].x) - mn2);
+      const h2_t p23 = exp2_h2(__builtin_bit_cast(h2_t, cur.s[p].y) - mn2);
+      const float ap[4] = {(float)p01[0], (float)p01[1], (float)p23[0], (float)p23[1]};
+      // P^ = HIF4(P) over the row's 64 keys
+      const float a4 = fmaxf(fmaxf(ap[0], ap[1]), fmaxf(ap[2], ap[3]));
+      const float a8 = fmaxf(a4, __shfl_xor(a4, 1));
+      float A = a8;
+#pragma unroll
+      for (int o = 2; o < 16; o <<= 1) A = fmaxf(A, __shfl_xor(A, o));
+      const uint32_t base = e6m2_ceil(A);
       const float bval = e6m2_value(base);
-      const float a8 = group_max(ap, 8), a4 = group_max(ap, 4);
       const bool e2 = a8 <= 0.875f * bval;
       const bool e3 = a4 <= (e2 ? 0.4375f : 0.875f) * bval;
       const int sh = (int)e2 + (int)e3;
-      const float ov = hif4_elem(ap, hif4_rcp_step(base), round_const(sh));   // u * 2^-sh
-      ph[r * 64 + lane] = ov * (0.25f * bval);
-      const float lsum = wave_sum(NORM == 0 ? ov * (0.25f * bval) : ap);
-      l[i] = l[i] * rr[i] + lsum;
+      const float R = hif4_rcp_step(base);
+      const float C = round_const(sh);
+      uint32_t u[4], v[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        u[j] = __float_as_uint(__builtin_fmaf(ap[j], R, C)) - __float_as_uint(C);   // round-half-away(a/step)
+        v[j] = u[j] << (2 - sh);
+        lp[r * 64 + 16 * quarter + operand_byte(4 * (kq & 3) + j)] = (uint8_t)v[j];
+      }
+      float ls;
+      if (NORM == 0) {
+        ls = (float)(v[0] + v[1] + v[2] + v[3]);
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) ls += __shfl_xor(ls, o);
+        ls *= bval * 0.0625f;                             // P^ = (4 u 2^-sh) * b/16
+      } else {
+        ls = (ap[0] + ap[1]) + (ap[2] + ap[3]);
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) ls += __shfl_xor(ls, o);
+      }
+      l[p] = l[p] * rr[p] + ls;
+      sp16[p] = bval * 0.0625f;
       if (DEBUG) {
-        const uint32_t u = (uint32_t)(ov * (float)(1 << sh));
-        const uint32_t hi = (uint32_t)__shfl_xor((int)u, 1);
-        const size_t dj = ((size_t)(hk * grp + r) * a.batch + b) * a.NB + J;
-        if ((lane & 1) == 0) a.dbg_codes[dj * 32 + (lane >> 1)] = (uint8_t)(u | (hi << 4));
         const uint64_t b2 = __ballot(e2), b3 = __ballot(e3);
-        if (lane == 0) {
-          uint32_t w2 = 0, w3 = 0;
-          for (int k = 0; k < 8; ++k) w2 |= (uint32_t)((b2 >> (8 * k)) & 1u) << k;
-          for (int q = 0; q < 16; ++q) w3 |= (uint32_t)((b3 >> (4 * q)) & 1u) << q;
-          a.dbg_meta[dj] = base | (w2 << 8) | (w3 << 16);
+        if (r < grp) {
+          const size_t dj = ((size_t)(hk * grp + r) * a.batch + b) * a.NB + J;
+          *reinterpret_cast<uint16_t*>(a.dbg_codes + dj * 32 + 2 * kq) =
+              (uint16_t)(u[0] | u[1] << 4 | u[2] << 8 | u[3] << 12);
+          if (kq == 0) {
+            const int l0 = lane & 48;
+            uint32_t w2 = 0, w3 = 0;
+            for (int k = 0; k < 8; ++k) w2 |= (uint32_t)((b2 >> (l0 + 2 * k)) & 1u) << k;
+            for (int k = 0; k < 16; ++k) w3 |= (uint32_t)((b3 >> (l0 + k)) & 1u) << k;
+            a.dbg_meta[dj] = base | (w2 << 8) | (w3 << 16);
+          }
         }
       }
     }
-    __syncthreads();
+    // A operands of row n, and the per-row factors of the output rows 4h + c
+    i4_t pa0 = {0, 0, 0, 0}, pa1 = {0, 0, 0, 0};
+    if (n < grp) {
+      pa0 = *reinterpret_cast<const i4_t*>(lp + n * 64 + 32 * h);
+      pa1 = *reinterpret_cast<const i4_t*>(lp + n * 64 + 32 * h + 16);
+    }
+    float rrc[4], spc[4];
 #pragma unroll
-    for (int i = 0; i < kMaxRowsPerWave; ++i) {
-      const int r = wave + 4 * i;
-      if (r >= grp) break;
-      const float* pr = ph + r * 64;
-#pragma unroll
-      for (int j = 0; j < kMaxChPerLane; ++j) {
-        if (64 * j >= D) break;
-        const int ch = lane + 64 * j;
-        float acc = 0.0f;
-#pragma unroll 16
-        for (int key = 0; key < 64; ++key) acc = __builtin_fmaf(pr[key], vv[key * D + ch], acc);
-        O[i][j] = __builtin_fmaf(O[i][j], rr[i], acc);
+    for (int c = 0; c < 4; ++c) {
+      rrc[c] = __shfl(rr[0], 16 * c);
+      spc[c] = __shfl(sp16[0], 16 * c);
+      if (RP > 1) {
+        const float r1 = __shfl(rr[RP - 1], 16 * c), s1 = __shfl(sp16[RP - 1], 16 * c);
+        if (h) {
+          rrc[c] = r1;
+          spc[c] = s1;
+        }
       }
     }
-    __syncthreads();
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const uint32_t meta = cur.meta[t];
+      const i16_t dot = group_dot(pa0, pa1, cur.w[t], meta, h);
+      const float sv = e6m2_value(meta & 255u) * 0.0625f;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) O[t][c] = __builtin_fmaf(O[t][c], rrc[c], (float)dot[c] * sv * spc[c]);
+    }
+  };
+#pragma unroll
+  for (int i = 0; i < kBlocksPerSplit; i += 2) {
+    if (J0 + i < J1) block(b0, J0 + i);
+    if (i + 2 < kBlocksPerSplit) load(min(J0 + i + 2, J1 - 1), b0);
+    if (J0 + i + 1 < J1) block(b1, J0 + i + 1);
+    if (i + 3 < kBlocksPerSplit) load(min(J0 + i + 3, J1 - 1), b1);
   }
 #pragma unroll
-  for (int i = 0; i < kMaxRowsPerWave; ++i) {
-    const int r = wave + 4 * i;
-    if (r >= grp) break;
-    const size_t row = (size_t)b * a.hq + hk * grp + r;
-    float* dst = a.opart + (row * a.n_split + sp) * D;
+  for (int c = 0; c < 4; ++c) {
+    const int r = 4 * h + c;
+    if (r < grp) {
+      float* dst = a.opart + ((row0 + r) * a.n_split + sp) * D + n;
 #pragma unroll
-    for (int j = 0; j < kMaxChPerLane; ++j)
-      if (64 * j < D) dst[lane + 64 * j] = O[i][j];
-    if (lane == 0) a.lpart[row * a.n_split + sp] = l[i];
+      for (int t = 0; t < NT; ++t) dst[32 * t] = O[t][c];
+    }
+  }
+#pragma unroll
+  for (int p = 0; p < RP; ++p) {
+    const int r = 4 * p + (lane >> 4);
+    if (r < grp && kq == 0) a.lpart[(row0 + r) * a.n_split + sp] = l[p];
   }
 }
 
 // ---------------------------------------------------------------------------
-// 3. Merge.  One wave per row (b, query head).  A forward pass over the block
-// maxima, 64 blocks at a time, gives the running maxima m_J (prefix maxima),
-// the factors r_J = E(fp16(m_{J-1} - m_J)) and their product over each split;
-// a backward pass over the splits turns those into R_s = the product over
-// all later splits.
-__global__ void __launch_bounds__(64) k_decode_merge(DecodeArgs a) {
-  extern __shared__ float R[];                    // [n_split]
+// 3. Merge.  One workgroup of four waves per row (b, query head).  Wave 0
+// walks the block maxima, 64 blocks at a time: the running maxima m_J
+// (prefix maxima), the factors r_J = E(fp16(m_{J-1} - m_J)) and their product
+// over each split; a backward pass over the splits turns those into R_s =
+// the product over all later splits.  Then thread (part, channel) sums its
+// share of the splits and the parts are added through LDS.
+constexpr int kMergeThreads = 256;
+
+__global__ void __launch_bounds__(kMergeThreads) k_decode_merge(DecodeArgs a) {
+  extern __shared__ float R[];                    // [n_split], then partial sums
+  __shared__ float m_final;
   const int row = blockIdx.x;                     // b * hq + head
   const int b = row / a.hq, head = row % a.hq;
   const int L = dseq_len(a.cu, b, a.S);
   const int nblk = (L + 63) >> 6;
   if (nblk == 0) return;
   const int ns = (nblk + kBlocksPerSplit - 1) / kBlocksPerSplit;
-  const int lane = threadIdx.x;
-  half_t carry = (half_t)(-__builtin_inff());
-  for (int J0 = 0; J0 < nblk; J0 += 64) {
-    const int J = J0 + lane;
-    float f = J < nblk ? (float)a.mx[(size_t)row * a.NB + J] : -__builtin_inff();
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int D = a.D;
+  const int parts = kMergeThreads / D;            // 1, 2 or 4 threads per channel
+  float* acc_s = R + a.n_split;                   // [parts][D] and [parts] l sums
+  float* mxs = acc_s + parts * D + parts;         // the row's block maxima [NB]
+  for (int j = tid; j < nblk; j += kMergeThreads) mxs[j] = (float)a.mx[(size_t)row * a.NB + j];
+  __syncthreads();
+  if (tid < 64) {
+    half_t carry = (half_t)(-__builtin_inff());
+    for (int J0 = 0; J0 < nblk; J0 += 64) {
+      const int J = J0 + lane;
+      float f = J < nblk ? mxs[J] : -__builtin_inff();
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const float t = __shfl_up(f, o);
-      if (lane >= o) f = fmaxf(f, t);
+      for (int o = 1; o < 64; o <<= 1) {
+        const float t = __shfl_up(f, o);
+        if (lane >= o) f = fmaxf(f, t);
+      }
+      const half_t incl = hmax((half_t)f, carry);
+      const float prevf = __shfl_up((float)incl, 1);
+      const half_t prev = lane == 0 ? carry : (half_t)prevf;
+      float p = J < nblk ? (float)exp2_h(prev - incl) : 1.0f;
+#pragma unroll
+      for (int o = 1; o < kBlocksPerSplit; o <<= 1) p *= __shfl_xor(p, o);
+      const int s = J / kBlocksPerSplit;
+      if (lane % kBlocksPerSplit == 0 && s < ns) R[s] = p;
+      carry = (half_t)__shfl((float)incl, 63);
     }
-    const half_t incl = hmax((half_t)f, carry);
-    const float prevf = __shfl_up((float)incl, 1);
-    const half_t prev = lane == 0 ? carry : (half_t)prevf;
-    float p = J < nblk ? (float)exp2_h(prev - incl) : 1.0f;
-    p *= __shfl_xor(p, 1);
-    p *= __shfl_xor(p, 2);
-    p *= __shfl_xor(p, 4);
-    const int s = (J0 >> 3) + (lane >> 3);
-    if ((lane & 7) == 0 && s < ns) R[s] = p;
-    carry = (half_t)__shfl((float)incl, 63);
+    float tail = 1.0f;
+    for (int s1 = ns; s1 > 0; s1 -= 64) {
+      const int s = s1 - 1 - lane;
+      const float v = s >= 0 ? R[s] : 1.0f;
+      float incl = v;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const float t = __shfl_up(incl, o);
+        if (lane >= o) incl *= t;
+      }
+      const float excl = __shfl_up(incl, 1);
+      if (s >= 0) R[s] = tail * (lane == 0 ? 1.0f : excl);
+      tail *= __shfl(incl, 63);
+    }
+    if (lane == 0) m_final = (float)carry;
   }
   __syncthreads();
-  float tail = 1.0f;
-  for (int s1 = ns; s1 > 0; s1 -= 64) {
-    const int s = s1 - 1 - lane;
-    const float v = s >= 0 ? R[s] : 1.0f;
-    float incl = v;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const float t = __shfl_up(incl, o);
-      if (lane >= o) incl *= t;
-    }
-    const float excl = __shfl_up(incl, 1);
-    if (s >= 0) R[s] = tail * (lane == 0 ? 1.0f : excl);
-    tail *= __shfl(incl, 63);
-  }
+  const int ch = tid % D, part = tid / D;
+  float acc = 0.0f, lacc = 0.0f;
+  const float* op = a.opart + (size_t)row * a.n_split * D + ch;
+#pragma unroll 8
+  for (int s = part; s < ns; s += parts) acc = __builtin_fmaf(op[(size_t)s * D], R[s], acc);
+  if (ch == 0)
+    for (int s = part; s < ns; s += parts) lacc = __builtin_fmaf(a.lpart[(size_t)row * a.n_split + s], R[s], lacc);
+  acc_s[part * D + ch] = acc;
+  if (ch == 0) acc_s[parts * D + part] = lacc;
   __syncthreads();
-  float lacc = 0.0f;
-  for (int s = lane; s < ns; s += 64) lacc = __builtin_fmaf(a.lpart[(size_t)row * a.n_split + s], R[s], lacc);
-  const float lsum = wave_sum(lacc);
-  const float inv = 1.0f / lsum;
-  for (int ch = lane; ch < a.D; ch += 64) {
-    float acc = 0.0f;
-    for (int s = 0; s < ns; ++s) acc = __builtin_fmaf(a.opart[((size_t)row * a.n_split + s) * a.D + ch], R[s], acc);
-    a.o[(size_t)row * a.D + ch] = (half_t)(acc * inv);
+  if (part == 0) {
+    float o = acc, lsum = 0.0f;
+    for (int p = 1; p < parts; ++p) o += acc_s[p * D + ch];
+    for (int p = 0; p < parts; ++p) lsum += acc_s[parts * D + p];
+    a.o[(size_t)row * D + ch] = (half_t)(o * (1.0f / lsum));
+    if (ch == 0) a.lse[(size_t)head * a.batch + b] = m_final * 0.69314718055994531f + logf(lsum);
   }
-  if (lane == 0) a.lse[(size_t)head * a.batch + b] = (float)carry * 0.69314718055994531f + logf(lsum);
 }
 
 void decode_offsets(int batch, int hq, int D, int NB, size_t off[7]) {
@@ -362,6 +569,24 @@ hipError_t allow_lds(K kern, size_t bytes) {
   if (bytes <= 65536) return hipSuccess;
   return hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
                              (int)bytes);
+}
+
+template <int NT, int RP>
+void launch_split(const DecodeArgs& a, int norm, bool debug, dim3 grid, dim3 block, hipStream_t st) {
+  if (norm == 0) {
+    if (debug) k_decode_split<NT, RP, 0, true><<<grid, block, 0, st>>>(a);
+    else k_decode_split<NT, RP, 0, false><<<grid, block, 0, st>>>(a);
+  } else {
+    if (debug) k_decode_split<NT, RP, 1, true><<<grid, block, 0, st>>>(a);
+    else k_decode_split<NT, RP, 1, false><<<grid, block, 0, st>>>(a);
+  }
+}
+
+template <int NT>
+void launch_split_rows(const DecodeArgs& a, int grp, int norm, bool debug, dim3 grid, dim3 block,
+                       hipStream_t st) {
+  if (grp <= 4) launch_split<NT, 1>(a, norm, debug, grid, block, st);
+  else launch_split<NT, 2>(a, norm, debug, grid, block, st);
 }
 
 }  // namespace
@@ -399,36 +624,34 @@ hipError_t launch_decode(const DecodeLaunch& d, hipStream_t st) {
   a.hkv = d.hkv;
   a.D = d.D;
   a.n_split = (d.NB + kBlocksPerSplit - 1) / kBlocksPerSplit;
+  a.waves = d.hkv < kMaxWaves ? d.hkv : kMaxWaves;
   a.c = d.c;
   const int grp = d.hq / d.hkv;
   hipError_t e = launch_quant_rows(d.q, d.s, ws + off[0], reinterpret_cast<uint32_t*>(ws + off[1]), d.batch, d.hq,
                                    d.hkv, d.D, false, st);
   if (e != hipSuccess) return e;
-  const size_t lds1 = (size_t)grp * d.D * sizeof(float);
-  k_decode_scores<<<dim3(d.NB, d.hkv, d.batch), dim3(256), lds1, st>>>(a);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  if (d.ev && (e = hipEventRecord(d.ev[1], st)) != hipSuccess) return e;
-  const size_t lds2 = ((size_t)64 * d.D + (size_t)grp * 64) * sizeof(float);
-  const dim3 g2(a.n_split, d.hkv, d.batch);
-  if (d.norm == 0) {
-    if (d.dbg_codes) {
-      if ((e = allow_lds(k_decode_split<0, true>, lds2)) != hipSuccess) return e;
-      k_decode_split<0, true><<<g2, dim3(256), lds2, st>>>(a);
-    } else {
-      if ((e = allow_lds(k_decode_split<0, false>, lds2)) != hipSuccess) return e;
-      k_decode_split<0, false><<<g2, dim3(256), lds2, st>>>(a);
-    }
-  } else {
-    if (d.dbg_codes) {
-      if ((e = allow_lds(k_decode_split<1, true>, lds2)) != hipSuccess) return e;
-      k_decode_split<1, true><<<g2, dim3(256), lds2, st>>>(a);
-    } else {
-      if ((e = allow_lds(k_decode_split<1, false>, lds2)) != hipSuccess) return e;
-      k_decode_split<1, false><<<g2, dim3(256), lds2, st>>>(a);
-    }
+  const dim3 block(64 * a.waves);
+  const int head_groups = (d.hkv + a.waves - 1) / a.waves;
+  const dim3 g1(head_groups, (d.NB + kScoreBlocksPerWave - 1) / kScoreBlocksPerWave, d.batch);
+  switch (d.D) {
+    case 64: k_decode_scores<1><<<g1, block, 0, st>>>(a); break;
+    case 128: k_decode_scores<2><<<g1, block, 0, st>>>(a); break;
+    default: k_decode_scores<4><<<g1, block, 0, st>>>(a); break;
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  k_decode_merge<<<dim3(d.batch * d.hq), dim3(64), (size_t)a.n_split * sizeof(float), st>>>(a);
+  if (d.ev && (e = hipEventRecord(d.ev[1], st)) != hipSuccess) return e;
+  const dim3 g2(head_groups, a.n_split, d.batch);
+  const bool dbg = d.dbg_codes != nullptr;
+  switch (d.D) {
+    case 64: launch_split_rows<2>(a, grp, d.norm, dbg, g2, block, st); break;
+    case 128: launch_split_rows<4>(a, grp, d.norm, dbg, g2, block, st); break;
+    default: launch_split_rows<8>(a, grp, d.norm, dbg, g2, block, st); break;
+  }
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  const int parts = kMergeThreads / d.D;
+  const size_t lds3 = ((size_t)a.n_split + (size_t)parts * d.D + parts + d.NB) * sizeof(float);
+  if ((e = allow_lds(k_decode_merge, lds3)) != hipSuccess) return e;
+  k_decode_merge<<<dim3(d.batch * d.hq), dim3(kMergeThreads), lds3, st>>>(a);
   return hipGetLastError();
 }
 

@@ -90,7 +90,7 @@ def test_decode_validation_codes(lib):
     assert "HIF4" in h.hifa4_last_error()
     assert _dec(lib, _p(), opt=h.FwdOptions(0, 0, 0, None, None, None, 1)) == -2  # Q-Mean
     assert "q_mean" in h.hifa4_last_error()
-    assert _dec(lib, _p(num_heads_q=32, num_heads_kv=2)) == -2                   # GQA group of 16
+    assert _dec(lib, _p(num_heads_q=64, num_heads_kv=2)) == -2                   # GQA group of 32
     assert _dec(lib, _p(), ptr=None) == -1
     assert _dec(lib, _p(), opt=h.FwdOptions(0, 0, 1, None, None, None)) == -1     # smooth without s
     assert _dec(lib, _p(), opt=h.FwdOptions(0, 0, 0, None, 1, None)) == -1        # half a debug dump
