@@ -194,7 +194,6 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (G <= 2 ? 4 : 2)) k_decode_sco
   // block), so the number of loads in flight is the same on every path
   KBlock b0, b1;
   load(J0, b0);
-  load(min(J0 + 1, J1 - 1), b1);
   i4_t qa[G][2];
   float wq[G][4];
 #pragma unroll
@@ -210,6 +209,7 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (G <= 2 ? 4 : 2)) k_decode_sco
       wq[g][c] = (0.25f * e6m2_value(mr & 255u)) * a.c;
     }
   }
+  load(min(J0 + 1, J1 - 1), b1);
   half_t* ls = &lds_s[wave][0][0];
   auto compute = [&](const KBlock& kb, int i) {
     const int J = J0 + i;
@@ -471,16 +471,18 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (NT <= 4 ? 4 : 2)) k_decode_sp
 }
 
 // ---------------------------------------------------------------------------
-// 3. Merge.  One workgroup of four waves per row (b, query head).  Wave 0
-// walks the block maxima, 64 blocks at a time: the running maxima m_J
-// (prefix maxima), the factors r_J = E(fp16(m_{J-1} - m_J)) and their product
-// over each split; a backward pass over the splits turns those into R_s =
-// the product over all later splits.  Then thread (part, channel) sums its
-// share of the splits and the parts are added through LDS.
-constexpr int kMergeThreads = 256;
+// 3. Merge.  One workgroup of four waves per row (b, query head).  The row's
+// block maxima are staged in LDS.  Wave 0 then takes 64 splits at a time,
+// lane = split: the split's own maximum, an exclusive prefix maximum over the
+// lanes (the running maximum entering the split), and a walk over the split's
+// blocks giving the product of their factors r_J = E(fp16(m_{J-1} - m_J)); a
+// backward pass over the splits turns those products into R_s = the product
+// over all later splits.  Thread (part, channel) then sums its share of the
+// splits and the parts are added through LDS.
+constexpr int kMergeThreads = 512;
 
 __global__ void __launch_bounds__(kMergeThreads) k_decode_merge(DecodeArgs a) {
-  extern __shared__ float R[];                    // [n_split], then partial sums
+  extern __shared__ float R[];                    // [n_split], then partial sums, then block maxima
   __shared__ float m_final;
   const int row = blockIdx.x;                     // b * hq + head
   const int b = row / a.hq, head = row % a.hq;
@@ -490,35 +492,49 @@ __global__ void __launch_bounds__(kMergeThreads) k_decode_merge(DecodeArgs a) {
   const int ns = (nblk + kBlocksPerSplit - 1) / kBlocksPerSplit;
   const int tid = threadIdx.x, lane = tid & 63;
   const int D = a.D;
-  const int parts = kMergeThreads / D;            // 1, 2 or 4 threads per channel
+  const int parts = kMergeThreads / D;            // 2, 4 or 8 threads per channel
   float* acc_s = R + a.n_split;                   // [parts][D] and [parts] l sums
   float* mxs = acc_s + parts * D + parts;         // the row's block maxima [NB]
   for (int j = tid; j < nblk; j += kMergeThreads) mxs[j] = (float)a.mx[(size_t)row * a.NB + j];
+  // the partial sums do not depend on the scan: load them first
+  const int ch = tid % D, part = tid / D;
+  constexpr int kMaxHeld = 16;
+  float po[kMaxHeld];
+  const float* op = a.opart + (size_t)row * a.n_split * D + ch;
+#pragma unroll
+  for (int k = 0; k < kMaxHeld; ++k) {
+    const int s = part + k * parts;
+    po[k] = s < ns ? op[(size_t)s * D] : 0.0f;
+  }
   __syncthreads();
   if (tid < 64) {
     half_t carry = (half_t)(-__builtin_inff());
-    for (int J0 = 0; J0 < nblk; J0 += 64) {
-      const int J = J0 + lane;
-      float f = J < nblk ? mxs[J] : -__builtin_inff();
+    for (int s0 = 0; s0 < ns; s0 += 64) {
+      const int sidx = s0 + lane;
+      const int j0 = sidx * kBlocksPerSplit, j1 = min(j0 + kBlocksPerSplit, nblk);
+      float lm = -__builtin_inff();
+      for (int j = j0; j < j1; ++j) lm = fmaxf(lm, mxs[j]);
+      float inc = lm;
 #pragma unroll
       for (int o = 1; o < 64; o <<= 1) {
-        const float t = __shfl_up(f, o);
-        if (lane >= o) f = fmaxf(f, t);
+        const float t = __shfl_up(inc, o);
+        if (lane >= o) inc = fmaxf(inc, t);
       }
-      const half_t incl = hmax((half_t)f, carry);
-      const float prevf = __shfl_up((float)incl, 1);
-      const half_t prev = lane == 0 ? carry : (half_t)prevf;
-      float p = J < nblk ? (float)exp2_h(prev - incl) : 1.0f;
-#pragma unroll
-      for (int o = 1; o < kBlocksPerSplit; o <<= 1) p *= __shfl_xor(p, o);
-      const int s = J / kBlocksPerSplit;
-      if (lane % kBlocksPerSplit == 0 && s < ns) R[s] = p;
-      carry = (half_t)__shfl((float)incl, 63);
+      const float exc = __shfl_up(inc, 1);
+      half_t m = lane == 0 ? carry : hmax((half_t)exc, carry);
+      float prod = 1.0f;
+      for (int j = j0; j < j1; ++j) {
+        const half_t mn = hmax(m, (half_t)mxs[j]);
+        prod *= (float)exp2_h(m - mn);
+        m = mn;
+      }
+      if (sidx < ns) R[sidx] = prod;
+      carry = hmax(carry, (half_t)__shfl(inc, 63));
     }
     float tail = 1.0f;
     for (int s1 = ns; s1 > 0; s1 -= 64) {
-      const int s = s1 - 1 - lane;
-      const float v = s >= 0 ? R[s] : 1.0f;
+      const int sidx = s1 - 1 - lane;
+      const float v = sidx >= 0 ? R[sidx] : 1.0f;
       float incl = v;
 #pragma unroll
       for (int o = 1; o < 64; o <<= 1) {
@@ -526,17 +542,19 @@ __global__ void __launch_bounds__(kMergeThreads) k_decode_merge(DecodeArgs a) {
         if (lane >= o) incl *= t;
       }
       const float excl = __shfl_up(incl, 1);
-      if (s >= 0) R[s] = tail * (lane == 0 ? 1.0f : excl);
+      if (sidx >= 0) R[sidx] = tail * (lane == 0 ? 1.0f : excl);
       tail *= __shfl(incl, 63);
     }
     if (lane == 0) m_final = (float)carry;
   }
   __syncthreads();
-  const int ch = tid % D, part = tid / D;
   float acc = 0.0f, lacc = 0.0f;
-  const float* op = a.opart + (size_t)row * a.n_split * D + ch;
-#pragma unroll 8
-  for (int s = part; s < ns; s += parts) acc = __builtin_fmaf(op[(size_t)s * D], R[s], acc);
+#pragma unroll
+  for (int k = 0; k < kMaxHeld; ++k) {
+    const int s = part + k * parts;
+    if (s < ns) acc = __builtin_fmaf(po[k], R[s], acc);
+  }
+  for (int s = part + kMaxHeld * parts; s < ns; s += parts) acc = __builtin_fmaf(op[(size_t)s * D], R[s], acc);
   if (ch == 0)
     for (int s = part; s < ns; s += parts) lacc = __builtin_fmaf(a.lpart[(size_t)row * a.n_split + s], R[s], lacc);
   acc_s[part * D + ch] = acc;
