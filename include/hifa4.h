@@ -18,6 +18,10 @@
  *   - Tensor pointers are DEVICE pointers owned by the caller; the library
  *     never allocates, frees or retains device memory, and keeps no device
  *     state between calls.  Where a host pointer is meant, it says so.
+ *   - Alignment: fp16 tensors (q, k, v, o), the scales s, HIF4 code buffers,
+ *     workspaces and debug code dumps 16 bytes; metadata buffers, LSE,
+ *     cu_seqlens and the calibration output 4 bytes.  Anything else fails with
+ *     HIFA4_ERR_INVALID_ARGUMENT before any work is enqueued.
  *   - Fixed-length problems use BSHD layout ([batch, seqlen, heads, dim],
  *     row-major, contiguous).  Variable-length problems pass cu_seqlens and
  *     use THD layout ([total_tokens, heads, dim]).

@@ -9,6 +9,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <initializer_list>
 #include <string>
 #include <vector>
 
@@ -38,6 +39,22 @@ struct Dims {
   int S;         // max_seqlen
   int NB;        // ceil(S/64)
 };
+
+// Vector loads and stores of the kernels need these alignments (a pointer
+// that may be NULL passes).
+bool aligned(const void* ptr, uintptr_t a) { return ((uintptr_t)ptr % a) == 0; }
+
+hifa4_status check_aligned16(std::initializer_list<const void*> ptrs) {
+  for (const void* ptr : ptrs)
+    if (!aligned(ptr, 16)) return fail(HIFA4_ERR_INVALID_ARGUMENT, "tensor pointer %p is not 16-byte aligned", ptr);
+  return HIFA4_OK;
+}
+
+hifa4_status check_aligned4(std::initializer_list<const void*> ptrs) {
+  for (const void* ptr : ptrs)
+    if (!aligned(ptr, 4)) return fail(HIFA4_ERR_INVALID_ARGUMENT, "pointer %p is not 4-byte aligned", ptr);
+  return HIFA4_OK;
+}
 
 hifa4_status check_problem(const hifa4_problem* p, Dims* d) {
   if (!p) return fail(HIFA4_ERR_INVALID_ARGUMENT, "problem is NULL");
@@ -87,6 +104,8 @@ hifa4_status hifa4_quantize_qk(const hifa4_problem* p, const void* q, const void
   const bool q_none = !q && !q_codes && !q_meta;
   if ((!q_none && (!q || !q_codes || !q_meta)) || !k || !k_codes || !k_meta)
     return fail(HIFA4_ERR_INVALID_ARGUMENT, "null tensor pointer");
+  if ((st = check_aligned16({q, k, s, q_codes, k_codes})) != HIFA4_OK) return st;
+  if ((st = check_aligned4({q_meta, k_meta, p->cu_seqlens})) != HIFA4_OK) return st;
   hipStream_t hs = (hipStream_t)stream;
   using hifa4::half_t;
   hipError_t e = hipSuccess;
@@ -106,6 +125,8 @@ hifa4_status hifa4_quantize_v(const hifa4_problem* p, const void* v, void* v_cod
   hifa4_status st = check_problem(p, &d);
   if (st != HIFA4_OK) return st;
   if (!v || !v_codes || !v_meta) return fail(HIFA4_ERR_INVALID_ARGUMENT, "null tensor pointer");
+  if ((st = check_aligned16({v, v_codes})) != HIFA4_OK) return st;
+  if ((st = check_aligned4({v_meta, p->cu_seqlens})) != HIFA4_OK) return st;
   hipError_t e = hifa4::launch_quant_v((const hifa4::half_t*)v, p->cu_seqlens, (uint8_t*)v_codes, (uint32_t*)v_meta,
                                        p->batch, d.S, d.NB, p->num_heads_kv, p->head_dim, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "quantize V");
@@ -127,6 +148,8 @@ hifa4_status hifa4_attention_fwd(const hifa4_problem* p, const hifa4_fwd_options
   if (!q || !k || !v || !o || !lse) return fail(HIFA4_ERR_INVALID_ARGUMENT, "null tensor pointer");
   if ((opt->debug_p_codes == nullptr) != (opt->debug_p_meta == nullptr))
     return fail(HIFA4_ERR_INVALID_ARGUMENT, "debug_p_codes and debug_p_meta must both be set or both be NULL");
+  if ((st = check_aligned16({q, k, v, o, s, workspace, opt->debug_p_codes})) != HIFA4_OK) return st;
+  if ((st = check_aligned4({lse, p->cu_seqlens, opt->debug_p_meta})) != HIFA4_OK) return st;
   // FP16 and P-only keep Q, K and V in fp16 (fp16 chunk layout, no smoothing)
   const bool fp16 = opt->operands != HIFA4_OPERANDS_HIF4;
   if (fp16 && opt->q_mean)
@@ -196,6 +219,8 @@ hifa4_status hifa4_decode_fwd(const hifa4_problem* p, const hifa4_fwd_options* o
     return fail(HIFA4_ERR_INVALID_ARGUMENT, "null tensor pointer");
   if ((opt->debug_p_codes == nullptr) != (opt->debug_p_meta == nullptr))
     return fail(HIFA4_ERR_INVALID_ARGUMENT, "debug_p_codes and debug_p_meta must both be set or both be NULL");
+  if ((st = check_aligned16({q, k_codes, v_codes, o, s, workspace, opt->debug_p_codes})) != HIFA4_OK) return st;
+  if ((st = check_aligned4({k_meta, v_meta, lse, p->cu_seqlens, opt->debug_p_meta})) != HIFA4_OK) return st;
   if (opt->smooth_qk && !s) return fail(HIFA4_ERR_INVALID_ARGUMENT, "smooth_qk set but s is NULL");
   if (d.tokens == 0 || d.S == 0) return HIFA4_OK;
   const size_t need = hifa4_decode_workspace_bytes(p);
@@ -250,6 +275,9 @@ hifa4_status hifa4_calibrate_smooth_qk(const hifa4_problem* p, int32_t n_calib, 
   if (p->head_dim != 64 && p->head_dim != 128 && p->head_dim != 256)
     return fail(HIFA4_ERR_UNSUPPORTED, "head_dim %d not in {64, 128, 256}", p->head_dim);
   if (!q_calib || !k_calib || !s_out) return fail(HIFA4_ERR_INVALID_ARGUMENT, "null tensor pointer");
+  hifa4_status st = check_aligned16({q_calib, k_calib, workspace});
+  if (st == HIFA4_OK) st = check_aligned4({s_out});
+  if (st != HIFA4_OK) return st;
   if (!std::isfinite(alpha) || alpha >= 1.0f) return fail(HIFA4_ERR_INVALID_ARGUMENT, "alpha must be finite and < 1");
   const size_t need = hifa4_calibrate_workspace_bytes(p, n_calib);
   if (!workspace || workspace_bytes < need)

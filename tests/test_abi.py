@@ -39,7 +39,10 @@ def _p(**kw):
     return h.Problem(**base)
 
 
-def _fwd(lib, p, opt=None, ptr=1, ws=1 << 30):
+FAKE = 1 << 12          # an aligned non-NULL address; never dereferenced (validation fails first)
+
+
+def _fwd(lib, p, opt=None, ptr=FAKE, ws=1 << 30):
     opt = opt or h.FwdOptions(0, 0, 0, None, None, None)
     return lib.hifa4_attention_fwd(ctypes.byref(p), ctypes.byref(opt), ptr, ptr, ptr, None, ptr, ptr,
                                    ptr, ws, None)
@@ -54,7 +57,7 @@ def test_validation_codes(lib):
     assert _fwd(lib, _p(), ptr=None) == -1
     assert _fwd(lib, _p(), opt=h.FwdOptions(7, 0, 0, None, None, None)) == -1
     assert _fwd(lib, _p(), opt=h.FwdOptions(0, 0, 1, None, None, None)) == -1      # smooth without s
-    assert _fwd(lib, _p(), opt=h.FwdOptions(0, 0, 0, 1, None, None)) == -1         # half a debug dump
+    assert _fwd(lib, _p(), opt=h.FwdOptions(0, 0, 0, FAKE, None, None)) == -1      # half a debug dump
     assert _fwd(lib, _p(), opt=h.FwdOptions(0, 1, 0, None, None, None, 1)) == -2   # Q-Mean with fp16 operands
     assert "q_mean" in h.hifa4_last_error()
     assert _fwd(lib, _p(), ws=16) == -3
@@ -78,7 +81,7 @@ def test_workspace_sizes(lib):
     assert lib.hifa4_workspace_bytes(ctypes.byref(_p(head_dim=80)), ctypes.byref(o)) == 0
 
 
-def _dec(lib, p, opt=None, ptr=1, ws=1 << 30):
+def _dec(lib, p, opt=None, ptr=FAKE, ws=1 << 30):
     opt = opt or h.FwdOptions(0, 0, 0, None, None, None)
     return lib.hifa4_decode_fwd(ctypes.byref(p), ctypes.byref(opt), ptr, ptr, ptr, ptr, ptr, None, ptr, ptr,
                                 ptr, ws, None)
@@ -93,7 +96,7 @@ def test_decode_validation_codes(lib):
     assert _dec(lib, _p(num_heads_q=64, num_heads_kv=2)) == -2                   # GQA group of 32
     assert _dec(lib, _p(), ptr=None) == -1
     assert _dec(lib, _p(), opt=h.FwdOptions(0, 0, 1, None, None, None)) == -1     # smooth without s
-    assert _dec(lib, _p(), opt=h.FwdOptions(0, 0, 0, None, 1, None)) == -1        # half a debug dump
+    assert _dec(lib, _p(), opt=h.FwdOptions(0, 0, 0, None, FAKE, None)) == -1     # half a debug dump
     assert _dec(lib, _p(), opt=h.FwdOptions(3, 0, 0, None, None, None)) == -1
     assert _dec(lib, _p(), ws=16) == -3
 
@@ -107,3 +110,24 @@ def test_decode_workspace_sizes(lib):
     want = 4096 + 512 + rows * 64 * 64 * 2 + rows * 64 * 2 + rows * 8 * 128 * 4 + rows * 8 * 4
     assert lib.hifa4_decode_workspace_bytes(ctypes.byref(p)) == want
     assert lib.hifa4_decode_workspace_bytes(ctypes.byref(_p(head_dim=80))) == 0
+
+
+def test_alignment_is_checked(lib):
+    """fp16 tensors, scales, code buffers, workspace and P^ dumps need 16-byte
+    alignment, metadata and LSE 4 bytes; violations fail before any launch."""
+    p = _p()
+    for bad in (FAKE + 2, FAKE + 8):
+        assert lib.hifa4_attention_fwd(ctypes.byref(p), ctypes.byref(h.FwdOptions(0, 0, 0, None, None, None)),
+                                       bad, FAKE, FAKE, None, FAKE, FAKE, FAKE, 1 << 30, None) == -1
+        assert "aligned" in h.hifa4_last_error()
+        assert lib.hifa4_attention_fwd(ctypes.byref(p), ctypes.byref(h.FwdOptions(0, 0, 0, None, None, None)),
+                                       FAKE, FAKE, FAKE, None, FAKE, FAKE, bad, 1 << 30, None) == -1    # workspace
+        assert lib.hifa4_decode_fwd(ctypes.byref(p), ctypes.byref(h.FwdOptions(0, 0, 0, None, None, None)),
+                                    FAKE, bad, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, 1 << 30, None) == -1
+        assert lib.hifa4_quantize_qk(ctypes.byref(p), FAKE, FAKE, None, FAKE, FAKE, bad, FAKE, None) == -1
+        assert lib.hifa4_quantize_v(ctypes.byref(p), FAKE, bad, FAKE, None) == -1
+    assert lib.hifa4_attention_fwd(ctypes.byref(p), ctypes.byref(h.FwdOptions(0, 0, 0, None, None, None)),
+                                   FAKE, FAKE, FAKE, None, FAKE, FAKE + 2, FAKE, 1 << 30, None) == -1    # LSE
+    assert lib.hifa4_quantize_v(ctypes.byref(p), FAKE, FAKE, FAKE + 2, None) == -1                    # meta
+    assert lib.hifa4_decode_fwd(ctypes.byref(p), ctypes.byref(h.FwdOptions(0, 0, 0, None, None, None)),
+                                FAKE, FAKE, FAKE + 1, FAKE, FAKE, None, FAKE, FAKE, FAKE, 1 << 30, None) == -1

@@ -69,6 +69,8 @@ def _decode_and_compare(h, qd, k, v, cu, s, max_seqlen, norm="preorder", seqs=No
         else:
             k_seq, v_seq = k[cu[b]:cu[b + 1]], v[cu[b]:cu[b + 1]]
         L = k_seq.shape[0]
+        if L == 0:
+            continue                                # an empty sequence has no decode row
         nb = -(-L // 64)
         for hk in (range(hkv) if kv_heads is None else kv_heads):
             for j, r in enumerate(_oracle_row(qd[b], k_seq, v_seq, s, hk, grp, norm)):
@@ -89,6 +91,7 @@ def _last_queries(q, cu):
     (64, 2, 2, (129, 511), 2, False),                 # no GQA, D=64
     (256, 8, 1, (200, 33), 3, True),                  # GQA x8 (two rows per wave), D=256
     (128, 6, 2, (150, 700), 4, True),                 # GQA x3 (one wave idle)
+    (128, 4, 1, (0, 300, 0, 65), 7, True),            # empty sequences (their rows are left untouched)
 ])
 def test_decode_varlen_parity(h, d, hq, hkv, lens, seed, smooth):
     q, k, v, cu = small_case(heads_q=hq, heads_kv=hkv, head_dim=d, seqlens=lens, seed=seed)
