@@ -126,7 +126,8 @@ struct DecodeArgs {
   half_t* s2;              // scores [batch, Hq, NB, 64]
   half_t* mx;              // block maxima [batch, Hq, NB]
   float* opart;            // [batch, Hq, n_split, D]
-  float* lpart;            // [batch, Hq, n_split]
+  float4* spart;           // [batch, Hq, n_split]: l, product of the split's
+                           // rescale factors, running max after its last block
   half_t* o;               // [batch, Hq, D]
   float* lse;              // [Hq, batch]
   uint8_t* dbg_codes;      // [Hq, batch, NB, 32] or null
@@ -327,11 +328,12 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (NT <= 4 ? 4 : 2)) k_decode_sp
   // the running maximum entering block J0 of each softmax row: the prefix
   // maximum of the block maxima, with every load of a row issued at once
   half_t m[RP];
-  float l[RP];
+  float l[RP], prod[RP];
 #pragma unroll
   for (int p = 0; p < RP; ++p) {
     m[p] = (half_t)(-__builtin_inff());
     l[p] = 0.0f;
+    prod[p] = 1.0f;
   }
   for (int r = 0; r < grp; ++r) {
     float pm = -__builtin_inff();
@@ -365,6 +367,7 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (NT <= 4 ? 4 : 2)) k_decode_sp
       // FP16 softmax of the lane's four keys
       const half_t mn = hmax(m[p], cur.mx[p]);
       rr[p] = (float)exp2_h(m[p] - mn);
+      prod[p] *= rr[p];
       m[p] = mn;
       const h2_t mn2 = {mn, mn};
       const h2_t p01 = exp2_h2(__builtin_bit_cast(h2_t, cur.s[p].x) - mn2);
@@ -466,24 +469,22 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (NT <= 4 ? 4 : 2)) k_decode_sp
 #pragma unroll
   for (int p = 0; p < RP; ++p) {
     const int r = 4 * p + (lane >> 4);
-    if (r < grp && kq == 0) a.lpart[(row0 + r) * a.n_split + sp] = l[p];
+    if (r < grp && kq == 0) a.spart[(row0 + r) * a.n_split + sp] = make_float4(l[p], prod[p], (float)m[p], 0.0f);
   }
 }
 
 // ---------------------------------------------------------------------------
-// 3. Merge.  One workgroup of four waves per row (b, query head).  The row's
-// block maxima are staged in LDS.  Wave 0 then takes 64 splits at a time,
-// lane = split: the split's own maximum, an exclusive prefix maximum over the
-// lanes (the running maximum entering the split), and a walk over the split's
-// blocks giving the product of their factors r_J = E(fp16(m_{J-1} - m_J)); a
-// backward pass over the splits turns those products into R_s = the product
-// over all later splits.  Thread (part, channel) then sums its share of the
-// splits and the parts are added through LDS.
+// 3. Merge.  One workgroup per row (b, query head).  Each split wrote its l,
+// the product of its blocks' rescale factors r_J = E(fp16(m_{J-1} - m_J))
+// (in block order) and its running maximum after its last block.  Wave 0
+// turns the products into R_s = the product over all later splits (a backward
+// scan, 64 splits at a time); the partial sums, loaded before the scan, are
+// then weighted and added, thread (part, channel) taking every parts-th
+// split, and the parts combined through LDS.
 constexpr int kMergeThreads = 512;
 
 __global__ void __launch_bounds__(kMergeThreads) k_decode_merge(DecodeArgs a) {
-  extern __shared__ float R[];                    // [n_split], then partial sums, then block maxima
-  __shared__ float m_final;
+  extern __shared__ float R[];                    // [n_split], then partial sums
   const int row = blockIdx.x;                     // b * hq + head
   const int b = row / a.hq, head = row % a.hq;
   const int L = dseq_len(a.cu, b, a.S);
@@ -494,8 +495,7 @@ __global__ void __launch_bounds__(kMergeThreads) k_decode_merge(DecodeArgs a) {
   const int D = a.D;
   const int parts = kMergeThreads / D;            // 2, 4 or 8 threads per channel
   float* acc_s = R + a.n_split;                   // [parts][D] and [parts] l sums
-  float* mxs = acc_s + parts * D + parts;         // the row's block maxima [NB]
-  for (int j = tid; j < nblk; j += kMergeThreads) mxs[j] = (float)a.mx[(size_t)row * a.NB + j];
+  const float4* sp = a.spart + (size_t)row * a.n_split;
   // the partial sums do not depend on the scan: load them first
   const int ch = tid % D, part = tid / D;
   constexpr int kMaxHeld = 16;
@@ -506,35 +506,11 @@ __global__ void __launch_bounds__(kMergeThreads) k_decode_merge(DecodeArgs a) {
     const int s = part + k * parts;
     po[k] = s < ns ? op[(size_t)s * D] : 0.0f;
   }
-  __syncthreads();
   if (tid < 64) {
-    half_t carry = (half_t)(-__builtin_inff());
-    for (int s0 = 0; s0 < ns; s0 += 64) {
-      const int sidx = s0 + lane;
-      const int j0 = sidx * kBlocksPerSplit, j1 = min(j0 + kBlocksPerSplit, nblk);
-      float lm = -__builtin_inff();
-      for (int j = j0; j < j1; ++j) lm = fmaxf(lm, mxs[j]);
-      float inc = lm;
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const float t = __shfl_up(inc, o);
-        if (lane >= o) inc = fmaxf(inc, t);
-      }
-      const float exc = __shfl_up(inc, 1);
-      half_t m = lane == 0 ? carry : hmax((half_t)exc, carry);
-      float prod = 1.0f;
-      for (int j = j0; j < j1; ++j) {
-        const half_t mn = hmax(m, (half_t)mxs[j]);
-        prod *= (float)exp2_h(m - mn);
-        m = mn;
-      }
-      if (sidx < ns) R[sidx] = prod;
-      carry = hmax(carry, (half_t)__shfl(inc, 63));
-    }
     float tail = 1.0f;
     for (int s1 = ns; s1 > 0; s1 -= 64) {
       const int sidx = s1 - 1 - lane;
-      const float v = sidx >= 0 ? R[sidx] : 1.0f;
+      const float v = sidx >= 0 ? sp[sidx].y : 1.0f;
       float incl = v;
 #pragma unroll
       for (int o = 1; o < 64; o <<= 1) {
@@ -545,7 +521,6 @@ __global__ void __launch_bounds__(kMergeThreads) k_decode_merge(DecodeArgs a) {
       if (sidx >= 0) R[sidx] = tail * (lane == 0 ? 1.0f : excl);
       tail *= __shfl(incl, 63);
     }
-    if (lane == 0) m_final = (float)carry;
   }
   __syncthreads();
   float acc = 0.0f, lacc = 0.0f;
@@ -556,7 +531,7 @@ __global__ void __launch_bounds__(kMergeThreads) k_decode_merge(DecodeArgs a) {
   }
   for (int s = part + kMaxHeld * parts; s < ns; s += parts) acc = __builtin_fmaf(op[(size_t)s * D], R[s], acc);
   if (ch == 0)
-    for (int s = part; s < ns; s += parts) lacc = __builtin_fmaf(a.lpart[(size_t)row * a.n_split + s], R[s], lacc);
+    for (int s = part; s < ns; s += parts) lacc = __builtin_fmaf(sp[s].x, R[s], lacc);
   acc_s[part * D + ch] = acc;
   if (ch == 0) acc_s[parts * D + part] = lacc;
   __syncthreads();
@@ -565,7 +540,7 @@ __global__ void __launch_bounds__(kMergeThreads) k_decode_merge(DecodeArgs a) {
     for (int p = 1; p < parts; ++p) o += acc_s[p * D + ch];
     for (int p = 0; p < parts; ++p) lsum += acc_s[parts * D + p];
     a.o[(size_t)row * D + ch] = (half_t)(o * (1.0f / lsum));
-    if (ch == 0) a.lse[(size_t)head * a.batch + b] = m_final * 0.69314718055994531f + logf(lsum);
+    if (ch == 0) a.lse[(size_t)head * a.batch + b] = sp[ns - 1].z * 0.69314718055994531f + logf(lsum);
   }
 }
 
@@ -578,7 +553,7 @@ void decode_offsets(int batch, int hq, int D, int NB, size_t off[7]) {
   off[2] = o; o += round_up256((size_t)batch * hq * NB * 64 * 2);            // scores
   off[3] = o; o += round_up256((size_t)batch * hq * NB * 2);                 // block maxima
   off[4] = o; o += round_up256((size_t)batch * hq * n_split * D * 4);        // partial O
-  off[5] = o; o += round_up256((size_t)batch * hq * n_split * 4);            // partial l
+  off[5] = o; o += round_up256((size_t)batch * hq * n_split * 16);           // l, factor product, max
   off[6] = o;
 }
 
@@ -630,7 +605,7 @@ hipError_t launch_decode(const DecodeLaunch& d, hipStream_t st) {
   a.s2 = reinterpret_cast<half_t*>(ws + off[2]);
   a.mx = reinterpret_cast<half_t*>(ws + off[3]);
   a.opart = reinterpret_cast<float*>(ws + off[4]);
-  a.lpart = reinterpret_cast<float*>(ws + off[5]);
+  a.spart = reinterpret_cast<float4*>(ws + off[5]);
   a.o = d.o;
   a.lse = d.lse;
   a.dbg_codes = d.dbg_codes;
@@ -667,7 +642,7 @@ hipError_t launch_decode(const DecodeLaunch& d, hipStream_t st) {
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const int parts = kMergeThreads / d.D;
-  const size_t lds3 = ((size_t)a.n_split + (size_t)parts * d.D + parts + d.NB) * sizeof(float);
+  const size_t lds3 = ((size_t)a.n_split + (size_t)parts * d.D + parts) * sizeof(float);
   if ((e = allow_lds(k_decode_merge, lds3)) != hipSuccess) return e;
   k_decode_merge<<<dim3(d.batch * d.hq), dim3(kMergeThreads), lds3, st>>>(a);
   return hipGetLastError();

@@ -104,10 +104,10 @@ def test_decode_validation_codes(lib):
 def test_decode_workspace_sizes(lib):
     # B=2, Hq=32, D=128, S=4096: Q^ 2*32*2*32 B + meta 2*32*2*4 B (each
     # rounded to 256 B), scores 2*32*64*64*2 B, block maxima 2*32*64*2 B,
-    # 8 splits of partial O (128 fp32) and l per row
+    # per row 8 splits of partial O (128 fp32) and (l, factor product, max)
     p = _p(batch=2, max_seqlen=4096, num_heads_q=32, num_heads_kv=8)
     rows = 2 * 32
-    want = 4096 + 512 + rows * 64 * 64 * 2 + rows * 64 * 2 + rows * 8 * 128 * 4 + rows * 8 * 4
+    want = 4096 + 512 + rows * 64 * 64 * 2 + rows * 64 * 2 + rows * 8 * 128 * 4 + rows * 8 * 16
     assert lib.hifa4_decode_workspace_bytes(ctypes.byref(p)) == want
     assert lib.hifa4_decode_workspace_bytes(ctypes.byref(_p(head_dim=80))) == 0
 

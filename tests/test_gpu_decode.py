@@ -188,3 +188,38 @@ def test_decode_b8_l32768_sampled(h):
     s, _ = osmooth.calibrate(qc, kc, w.heads_kv, w.alpha)
     _say("decode_b8_l32768 sampled")
     _decode_and_compare(h, qd, k, v, None, s, w.seqlen, seqs=[0, 7], kv_heads=[0, 5])
+
+
+def test_decode_graph_replay(h):
+    """The decode step captured as a HIP graph: every replay, with eager work
+    and synchronizations between replays, equals the eager call bit for bit
+    (the library's launches record no memsets)."""
+    import torch
+    q, k, v, cu = small_case(heads_q=4, heads_kv=2, head_dim=128, seqlens=(700, 65), seed=13)
+    s = np.exp(np.random.default_rng(13).uniform(-1, 1, (2, 128))).astype(np.float32)
+    kc, km, vc, vm, cu_t = _build_cache(h, k, v, s, cu, 700)
+    qd, s_t = to_gpu(_last_queries(q, cu)), to_gpu(s)
+    ws = h.Workspace()
+    o_ref, l_ref = h.hifa4_decode_fwd(qd, kc, km, vc, vm, s_t, cu_seqlens=cu_t, max_seqlen=700, workspace=ws)
+    o_ref, l_ref = o_ref.clone(), l_ref.clone()
+    out = torch.empty_like(o_ref)
+    lse = torch.empty_like(l_ref)
+    kw = dict(cu_seqlens=cu_t, max_seqlen=700, workspace=ws, out=out, lse=lse)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        h.hifa4_decode_fwd(qd, kc, km, vc, vm, s_t, **kw)
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        h.hifa4_decode_fwd(qd, kc, km, vc, vm, s_t, **kw)
+    for i in range(4):
+        out.zero_()
+        lse.zero_()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, o_ref), i
+        assert torch.equal(lse, l_ref), i
+        h.hifa4_decode_fwd(qd, kc, km, vc, vm, s_t, cu_seqlens=cu_t, max_seqlen=700)   # eager work between
+        torch.cuda.synchronize()
+    _say("decode graph replays ok")
