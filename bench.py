@@ -305,6 +305,68 @@ def time_variant(h, torch, args, q, k, v, s, norm, operands, steps, warmup, ws, 
     return wall, sum(pre) / steps, sum(att) / steps, out, lse
 
 
+def call_distribution(h, torch, np, q, k, v, s, ws, steps=100, cold_steps=20):
+    """Device time per call (the library's events before the pre-pass and
+    after the attention kernel): median, p10 and p90 over back-to-back calls
+    with warm caches, then the median over calls that each follow a 512 MiB
+    scrub write (L2 and the 256 MB MALL evicted)."""
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    for trio in evs:
+        for e in trio:
+            e.record()
+    out = torch.empty_like(q)
+    lse = torch.empty((q.shape[2], q.shape[0] * q.shape[1]), dtype=torch.float32, device=q.device)
+    kw = dict(s=s, smooth_qk=s is not None, workspace=ws, out=out, lse=lse)
+    for _ in range(10):
+        h.hifa4_attention_fwd(q, k, v, **kw)
+    torch.cuda.synchronize()
+    for i in range(steps):
+        h.hifa4_attention_fwd(q, k, v, timing_events=evs[i], **kw)
+    torch.cuda.synchronize()
+    warm = np.array([e[0].elapsed_time(e[2]) for e in evs]) * 1e3
+    scrub = torch.empty(512 << 20, dtype=torch.uint8, device=q.device)
+    cold = []
+    for i in range(cold_steps):
+        scrub.fill_(i & 255)
+        h.hifa4_attention_fwd(q, k, v, timing_events=evs[i], **kw)
+        torch.cuda.synchronize()
+        cold.append(evs[i][0].elapsed_time(evs[i][2]) * 1e3)
+    del scrub
+    return {"unit": "us", "warm_median": round(float(np.median(warm)), 2),
+            "warm_p10": round(float(np.percentile(warm, 10)), 2), "warm_p90": round(float(np.percentile(warm, 90)), 2),
+            "cold_median": round(float(np.median(cold)), 2), "warm_steps": steps, "cold_steps": cold_steps}
+
+
+def observed_sclk(h, torch, q, k, v, s, ws, seconds=1.0):
+    """GPU core clock read with rocm-smi (a child process) half way through a
+    second of back-to-back forward calls; None if the tool is unavailable."""
+    import re
+    import subprocess
+    import threading
+    box = {}
+
+    def probe():
+        time.sleep(seconds / 2)
+        try:
+            import shutil
+            tool = shutil.which("rocm-smi") or "/opt/rocm/bin/rocm-smi"
+            r = subprocess.run([tool, "--showclocks"], capture_output=True, text=True, timeout=20)
+            m = re.search(r"sclk[^(]*\((\d+)\s*Mhz\)", r.stdout, re.IGNORECASE)
+            box["mhz"] = int(m.group(1)) if m else None
+        except Exception:
+            box["mhz"] = None
+
+    t = threading.Thread(target=probe)
+    t.start()
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(10):
+            h.hifa4_attention_fwd(q, k, v, s, workspace=ws)
+        torch.cuda.synchronize()
+    t.join()
+    return box.get("mhz")
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -410,6 +472,8 @@ def main():
                      "source_sha256": source_digest()},
         "paper_context": PAPER_CONTEXT,
         "clock_settle_calls": settle,
+        "call_device_time": call_distribution(h, torch, np, q, k, v, s, ws),
+        "sclk_mhz_during_calls": observed_sclk(h, torch, q, k, v, s, ws),
     }
     if not args.no_variants:
         wall16, pre16, att16, out16, _ = time_variant(h, torch, args, q, k, v, None, h.NORM_PREORDER,
