@@ -92,6 +92,7 @@ def _last_queries(q, cu):
     (256, 8, 1, (200, 33), 3, True),                  # GQA x8 (two rows per wave), D=256
     (128, 6, 2, (150, 700), 4, True),                 # GQA x3 (one wave idle)
     (128, 4, 1, (0, 300, 0, 65), 7, True),            # empty sequences (their rows are left untouched)
+    (64, 24, 12, (100, 37), 8, True),                 # 12 kv heads: two workgroups per key range
 ])
 def test_decode_varlen_parity(h, d, hq, hkv, lens, seed, smooth):
     q, k, v, cu = small_case(heads_q=hq, heads_kv=hkv, head_dim=d, seqlens=lens, seed=seed)
