@@ -142,6 +142,8 @@ def test_tiny_config_full_parity(h):
     (64, 2, 2, (129, 511), 2),                   # no GQA, D=64
     (256, 4, 2, (200, 33), 3),                   # GQA x2, D=256
     (128, 8, 8, (97,), 4),
+    (128, 16, 2, (150, 70), 6),                 # GQA x8: two workgroups of four heads per kv head
+    (64, 6, 2, (100, 33), 7),                    # GQA x3: one head per workgroup, 128-row tiles
 ])
 def test_varlen_parity(h, d, hq, hkv, lens, seed):
     q, k, v, cu = small_case(heads_q=hq, heads_kv=hkv, head_dim=d, seqlens=lens, seed=seed)
