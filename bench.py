@@ -69,6 +69,32 @@ def read_counters(name: str):
         return None
 
 
+# Plain (non-packed) VALU issue rate: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
+# lane-operations per second.  The datasheet's 157.3 TFLOP/s fp32 vector peak
+# is this rate x 2 (an FMA counts two FLOPs) x 2 (packed FP32, disabled here).
+PEAK_VALU_TLANEOPS = 256 * 4 * 16 * 2.4e9 / 1e12
+
+
+def read_sq_valu(name: str):
+    """Non-MFMA VALU instructions per dispatch of the attention kernel from a
+    committed SQ counter summary taken on the current kernel sources (else
+    None)."""
+    path = os.path.join(ROOT, "profiles", name)
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            vals[k.strip()] = v.strip()
+    if vals.get("source_sha256") != source_digest():
+        return None
+    try:
+        return float(vals["SQ_INSTS_VALU"]) - float(vals["SQ_INSTS_MFMA"])
+    except (KeyError, ValueError):
+        return None
+
+
 def cpu_baseline(w, q, k, v, s, n_heads):
     """The oracle as it stands, on the first n_heads query heads (whole KV
     groups, all rows) of the same inputs."""
@@ -305,6 +331,18 @@ def time_variant(h, torch, args, q, k, v, s, norm, operands, steps, warmup, ws, 
     return wall, sum(pre) / steps, sum(att) / steps, out, lse
 
 
+def valu_roofline(valu_insts, att_ms):
+    """The attention kernel against its practical bound, plain VALU issue:
+    non-MFMA VALU instructions per dispatch (SQ counters) x 64 lanes / the
+    live mean kernel time, against PEAK_VALU_TLANEOPS."""
+    if valu_insts is None:
+        return None
+    achieved = valu_insts * 64 / (att_ms * 1e-3) / 1e12
+    return {"bound": "alu", "achieved": round(achieved, 2), "peak": round(PEAK_VALU_TLANEOPS, 2),
+            "unit": "T VALU lane-ops/s", "frac": round(achieved / PEAK_VALU_TLANEOPS, 4),
+            "valu_instructions_per_dispatch": valu_insts}
+
+
 def call_distribution(h, torch, np, q, k, v, s, ws, steps=100, cold_steps=20):
     """Device time per call (the library's events before the pre-pass and
     after the attention kernel): median, p10 and p90 over back-to-back calls
@@ -472,6 +510,7 @@ def main():
                      "source_sha256": source_digest()},
         "paper_context": PAPER_CONTEXT,
         "clock_settle_calls": settle,
+        "valu_roofline": valu_roofline(read_sq_valu(f"attn_hif4_{w.name}_sq_counters.txt"), att_ms),
         "call_device_time": call_distribution(h, torch, np, q, k, v, s, ws),
         "sclk_mhz_during_calls": observed_sclk(h, torch, q, k, v, s, ws),
     }
