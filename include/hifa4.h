@@ -272,7 +272,8 @@ size_t hifa4_decode_workspace_bytes(const hifa4_problem* p);
  *    timing_events (before the query quantization, between the score kernel
  *    and the split kernel, after the merge) as for hifa4_attention_fwd; operands must be
  *    HIFA4_OPERANDS_HIF4 and q_mean 0 (the cache carries no key sums), else
- *    HIFA4_ERR_UNSUPPORTED; num_heads_q / num_heads_kv must be <= 16.
+ *    HIFA4_ERR_UNSUPPORTED; num_heads_q / num_heads_kv must be <= 8 (else
+ *    HIFA4_ERR_UNSUPPORTED).
  * workspace: DEVICE, >= hifa4_decode_workspace_bytes(p).  Asynchronous. */
 hifa4_status hifa4_decode_fwd(const hifa4_problem* p, const hifa4_fwd_options* opt,
                               const void* q, const void* k_codes, const void* k_meta,

@@ -196,7 +196,7 @@ hifa4_status hifa4_attention_fwd(const hifa4_problem* p, const hifa4_fwd_options
 size_t hifa4_decode_workspace_bytes(const hifa4_problem* p) {
   Dims d;
   if (check_problem(p, &d) != HIFA4_OK) return 0;
-  return hifa4::decode_workspace_bytes(p->batch, p->num_heads_q, p->head_dim, std::max(1, d.NB));
+  return hifa4::decode_workspace_bytes(p->batch, p->num_heads_q, p->num_heads_kv, p->head_dim, std::max(1, d.NB));
 }
 
 hifa4_status hifa4_decode_fwd(const hifa4_problem* p, const hifa4_fwd_options* opt, const void* q,
@@ -212,8 +212,8 @@ hifa4_status hifa4_decode_fwd(const hifa4_problem* p, const hifa4_fwd_options* o
   if (opt->operands != HIFA4_OPERANDS_HIF4)
     return fail(HIFA4_ERR_UNSUPPORTED, "decode reads a HIF4 cache: operands must be HIFA4_OPERANDS_HIF4");
   if (opt->q_mean) return fail(HIFA4_ERR_UNSUPPORTED, "q_mean is not supported by decode (the cache has no key sums)");
-  if (p->num_heads_q / p->num_heads_kv > 16)
-    return fail(HIFA4_ERR_UNSUPPORTED, "decode supports at most 16 query heads per kv head (got %d)",
+  if (p->num_heads_q / p->num_heads_kv > 8)
+    return fail(HIFA4_ERR_UNSUPPORTED, "decode supports at most 8 query heads per kv head (got %d)",
                 p->num_heads_q / p->num_heads_kv);
   if (!q || !k_codes || !k_meta || !v_codes || !v_meta || !o || !lse)
     return fail(HIFA4_ERR_INVALID_ARGUMENT, "null tensor pointer");

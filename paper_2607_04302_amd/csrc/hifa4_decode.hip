@@ -45,6 +45,7 @@
 // share cache lines, so the lines are read once by one compute unit.
 #include "hifa4_device.h"
 #include "hifa4_internal.h"
+#include "hifa4_packed.h"
 
 namespace hifa4 {
 
@@ -54,8 +55,16 @@ typedef int i4_t __attribute__((ext_vector_type(4)));
 typedef int i16_t __attribute__((ext_vector_type(16)));
 typedef unsigned short u16x2_t __attribute__((ext_vector_type(2)));
 
-constexpr int kScoreBlocksPerWave = 8;
-constexpr int kBlocksPerSplit = 8;       // a power of two <= 64
+// Blocks per score wave: 8 when that still gives at least two workgroups per
+// compute unit, else 2, else 1 (short or single sequences).  Blocks per split:
+// the longest of 8, 4 and 2 that gives a workgroup per compute unit, with at
+// most 128 splits per row, since every split also pays a prefix maximum over
+// the blocks before it, a partial output in fp32 and its share of the merge.
+constexpr int kScoreRuns[3] = {8, 2, 1};
+constexpr int kSplitLengths[3] = {8, 4, 2};
+constexpr int kMinScoreWorkgroups = 512;
+constexpr int kMinSplitWorkgroups = 256;
+constexpr int kMaxSplitsPerRow = 128;
 constexpr int kMaxWaves = 8;             // kv heads per workgroup
 
 __device__ __forceinline__ int dseq_start(const int* cu, int b, int S) { return cu ? cu[b] : b * S; }
@@ -124,7 +133,7 @@ struct DecodeArgs {
   const uint32_t* vm;      // [batch, NB, Hkv, D]
   const int* cu;
   half_t* s2;              // scores [batch, Hq, NB, 64]
-  half_t* mx;              // block maxima [batch, Hq, NB]
+  half_t* mx;              // block maxima [batch, Hq, mxs]
   float* opart;            // [batch, Hq, n_split, D]
   float4* spart;           // [batch, Hq, n_split]: l, product of the split's
                            // rescale factors, running max after its last block
@@ -132,7 +141,8 @@ struct DecodeArgs {
   float* lse;              // [Hq, batch]
   uint8_t* dbg_codes;      // [Hq, batch, NB, 32] or null
   uint32_t* dbg_meta;      // [Hq, batch, NB]
-  int batch, S, NB, hq, hkv, D, n_split, waves;
+  int batch, S, NB, hq, hkv, D, n_split, waves, bps;
+  int mxs;                 // row stride of the block maxima: NB rounded up to 8
   float c;
 };
 
@@ -147,8 +157,9 @@ struct DecodeArgs {
 // roles keep the next two blocks' codes in flight; the scores and maxima of
 // the run are collected in LDS and stored after the last block, so the loop
 // issues loads only.
-template <int G>
+template <int G, int RUN>
 __global__ void __launch_bounds__(64 * kMaxWaves, (G <= 2 ? 4 : 2)) k_decode_scores(DecodeArgs a) {
+  constexpr int kScoreBlocksPerWave = RUN;
   __shared__ __align__(16) half_t lds_s[kMaxWaves][8][kScoreBlocksPerWave * 64];
   __shared__ half_t lds_m[kMaxWaves][8][kScoreBlocksPerWave];
   const int wave = (int)(threadIdx.x >> 6);
@@ -252,7 +263,7 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (G <= 2 ? 4 : 2)) k_decode_sco
   for (int i = 0; i < kScoreBlocksPerWave; i += 2) {
     if (J0 + i < J1) compute(b0, i);
     if (i + 2 < kScoreBlocksPerWave) load(min(J0 + i + 2, J1 - 1), b0);
-    if (J0 + i + 1 < J1) compute(b1, i + 1);
+    if (i + 1 < kScoreBlocksPerWave && J0 + i + 1 < J1) compute(b1, i + 1);
     if (i + 3 < kScoreBlocksPerWave) load(min(J0 + i + 3, J1 - 1), b1);
   }
   // the run's scores (J1 - J0 blocks of 64, contiguous per row) and maxima
@@ -261,7 +272,7 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (G <= 2 ? 4 : 2)) k_decode_sco
     const uint2* src = reinterpret_cast<const uint2*>(ls + r * (kScoreBlocksPerWave * 64));
     uint2* dst = reinterpret_cast<uint2*>(a.s2 + ((row0 + r) * a.NB + J0) * 64);
     for (int k = lane; k < nb * 16; k += 64) dst[k] = src[k];
-    if (lane < nb) a.mx[(row0 + r) * a.NB + J0 + lane] = lds_m[wave][r][lane];
+    if (lane < nb) a.mx[(row0 + r) * a.mxs + J0 + lane] = lds_m[wave][r][lane];
   }
 }
 
@@ -274,8 +285,9 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (G <= 2 ? 4 : 2)) k_decode_sco
 // from where lane (row l & 31, half h) reads its two operands.  B = 32
 // channels of the block's V^ groups; per 32-channel tile the two MFMAs give
 // the exact block sums, and O[row][ch] = fma(O, r_row, dot * b_V/16 * b_P/16).
-template <int NT, int RP, int NORM, bool DEBUG>
-__global__ void __launch_bounds__(64 * kMaxWaves, (NT <= 4 ? 4 : 2)) k_decode_split(DecodeArgs a) {
+template <int NT, int RP, int NORM, bool DEBUG, int BPS>
+__global__ void __launch_bounds__(64 * kMaxWaves, (NT * RP <= 4 ? 4 : 2)) k_decode_split(DecodeArgs a) {
+  constexpr int kBlocksPerSplit = BPS;
   constexpr int D = 32 * NT;
   __shared__ __align__(16) uint8_t lds_p[kMaxWaves][8 * 64];
   const int wave = (int)(threadIdx.x >> 6);
@@ -317,7 +329,7 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (NT <= 4 ? 4 : 2)) k_decode_sp
     for (int p = 0; p < RP; ++p) {
       const size_t rj = (row0 + prow[p]) * a.NB + J;
       vb.s[p] = *reinterpret_cast<const uint2*>(a.s2 + rj * 64 + 4 * kq);
-      vb.mx[p] = a.mx[rj];
+      vb.mx[p] = a.mx[(row0 + prow[p]) * a.mxs + J];
     }
   };
   // every prefetch is unconditional (past the split's end it reloads the last
@@ -326,33 +338,51 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (NT <= 4 ? 4 : 2)) k_decode_sp
   load(J0, b0);
   load(min(J0 + 1, J1 - 1), b1);
   // the running maximum entering block J0 of each softmax row: the prefix
-  // maximum of the block maxima, with every load of a row issued at once
+  // maximum of the row's block maxima.  The 16 lanes of a row read 8 maxima
+  // per load; every load of a round is issued before the first is used.
+  constexpr int kPrefixLoads = 4 / RP;
   half_t m[RP];
   float l[RP], prod[RP];
+  h2_t pm[RP];
 #pragma unroll
   for (int p = 0; p < RP; ++p) {
-    m[p] = (half_t)(-__builtin_inff());
     l[p] = 0.0f;
     prod[p] = 1.0f;
+    pm[p] = h2_t{(half_t)(-__builtin_inff()), (half_t)(-__builtin_inff())};
   }
-  for (int r = 0; r < grp; ++r) {
-    float pm = -__builtin_inff();
-    for (int j0 = 0; j0 < J0; j0 += 64 * 8) {
-      half_t v[8];
+  const int nch = (J0 + 7) >> 3;                 // chunks of 8 maxima before J0
+  for (int c0 = 0; c0 < nch; c0 += 16 * kPrefixLoads) {
+    uint4 w[RP][kPrefixLoads];
+    int nv[kPrefixLoads];
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const int j = j0 + 64 * k + lane;
-        v[k] = a.mx[(row0 + r) * a.NB + (j < J0 ? j : 0)];
-      }
+    for (int k = 0; k < kPrefixLoads; ++k) {
+      const int c = c0 + 16 * k + kq;
+      const int ce = c < nch ? c : 0;            // past the end: chunk 0 again (max is idempotent)
+      nv[k] = J0 - 8 * ce;                       // maxima of the chunk before J0
 #pragma unroll
-      for (int k = 0; k < 8; ++k)
-        if (j0 + 64 * k + lane < J0) pm = fmaxf(pm, (float)v[k]);
+      for (int p = 0; p < RP; ++p)
+        w[p][k] = *reinterpret_cast<const uint4*>(a.mx + (row0 + prow[p]) * a.mxs + 8 * ce);
     }
 #pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) pm = fmaxf(pm, __shfl_xor(pm, o));
+    for (int k = 0; k < kPrefixLoads; ++k)
 #pragma unroll
-    for (int p = 0; p < RP; ++p)
-      if (4 * p + (lane >> 4) == r) m[p] = (half_t)pm;
+      for (int p = 0; p < RP; ++p) {
+        const uint32_t x[4] = {w[p][k].x, w[p][k].y, w[p][k].z, w[p][k].w};
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+          uint32_t v = x[d];
+          if (2 * d + 1 >= nv[k]) v = (v & 0xFFFFu) | 0xFC000000u;     // -inf
+          if (2 * d >= nv[k]) v = 0xFC00FC00u;
+          pm[p] = hmax2(pm[p], __builtin_bit_cast(h2_t, v));
+        }
+      }
+  }
+#pragma unroll
+  for (int p = 0; p < RP; ++p) {
+    float mm = fmaxf((float)pm[p][0], (float)pm[p][1]);
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) mm = fmaxf(mm, __shfl_xor(mm, o));
+    m[p] = (half_t)mm;
   }
   float O[NT][4];
 #pragma unroll
@@ -454,7 +484,7 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (NT <= 4 ? 4 : 2)) k_decode_sp
   for (int i = 0; i < kBlocksPerSplit; i += 2) {
     if (J0 + i < J1) block(b0, J0 + i);
     if (i + 2 < kBlocksPerSplit) load(min(J0 + i + 2, J1 - 1), b0);
-    if (J0 + i + 1 < J1) block(b1, J0 + i + 1);
+    if (i + 1 < kBlocksPerSplit && J0 + i + 1 < J1) block(b1, J0 + i + 1);
     if (i + 3 < kBlocksPerSplit) load(min(J0 + i + 3, J1 - 1), b1);
   }
 #pragma unroll
@@ -490,7 +520,7 @@ __global__ void __launch_bounds__(kMergeThreads) k_decode_merge(DecodeArgs a) {
   const int L = dseq_len(a.cu, b, a.S);
   const int nblk = (L + 63) >> 6;
   if (nblk == 0) return;
-  const int ns = (nblk + kBlocksPerSplit - 1) / kBlocksPerSplit;
+  const int ns = (nblk + a.bps - 1) / a.bps;
   const int tid = threadIdx.x, lane = tid & 63;
   const int D = a.D;
   const int parts = kMergeThreads / D;            // 2, 4 or 8 threads per channel
@@ -544,14 +574,33 @@ __global__ void __launch_bounds__(kMergeThreads) k_decode_merge(DecodeArgs a) {
   }
 }
 
-void decode_offsets(int batch, int hq, int D, int NB, size_t off[7]) {
+int pick_run(int head_groups, int batch, int NB) {
+  for (int run : kScoreRuns)
+    if ((long)head_groups * batch * ((NB + run - 1) / run) >= kMinScoreWorkgroups) return run;
+  return 1;
+}
+
+int pick_split(int head_groups, int batch, int NB) {
+  int pick = kSplitLengths[0];
+  for (int bps : kSplitLengths) {
+    const int n_split = (NB + bps - 1) / bps;
+    if (bps != kSplitLengths[0] && n_split > kMaxSplitsPerRow) break;
+    pick = bps;
+    if ((long)head_groups * batch * n_split >= kMinSplitWorkgroups) break;
+  }
+  return pick;
+}
+
+int maxima_stride(int NB) { return (NB + 7) & ~7; }
+
+void decode_offsets(int batch, int hq, int D, int NB, int bps, size_t off[7]) {
   const int G = D / 64;
-  const int n_split = (NB + kBlocksPerSplit - 1) / kBlocksPerSplit;
+  const int n_split = (NB + bps - 1) / bps;
   size_t o = 0;
   off[0] = o; o += round_up256((size_t)batch * hq * G * 32);                 // Q^ codes
   off[1] = o; o += round_up256((size_t)batch * hq * G * 4);                  // Q^ metadata
   off[2] = o; o += round_up256((size_t)batch * hq * NB * 64 * 2);            // scores
-  off[3] = o; o += round_up256((size_t)batch * hq * NB * 2);                 // block maxima
+  off[3] = o; o += round_up256((size_t)batch * hq * maxima_stride(NB) * 2);  // block maxima
   off[4] = o; o += round_up256((size_t)batch * hq * n_split * D * 4);        // partial O
   off[5] = o; o += round_up256((size_t)batch * hq * n_split * 16);           // l, factor product, max
   off[6] = o;
@@ -564,35 +613,61 @@ hipError_t allow_lds(K kern, size_t bytes) {
                              (int)bytes);
 }
 
-template <int NT, int RP>
+template <int NT, int RP, int BPS>
 void launch_split(const DecodeArgs& a, int norm, bool debug, dim3 grid, dim3 block, hipStream_t st) {
   if (norm == 0) {
-    if (debug) k_decode_split<NT, RP, 0, true><<<grid, block, 0, st>>>(a);
-    else k_decode_split<NT, RP, 0, false><<<grid, block, 0, st>>>(a);
+    if (debug) k_decode_split<NT, RP, 0, true, BPS><<<grid, block, 0, st>>>(a);
+    else k_decode_split<NT, RP, 0, false, BPS><<<grid, block, 0, st>>>(a);
   } else {
-    if (debug) k_decode_split<NT, RP, 1, true><<<grid, block, 0, st>>>(a);
-    else k_decode_split<NT, RP, 1, false><<<grid, block, 0, st>>>(a);
+    if (debug) k_decode_split<NT, RP, 1, true, BPS><<<grid, block, 0, st>>>(a);
+    else k_decode_split<NT, RP, 1, false, BPS><<<grid, block, 0, st>>>(a);
   }
 }
 
-template <int NT>
+template <int NT, int BPS>
 void launch_split_rows(const DecodeArgs& a, int grp, int norm, bool debug, dim3 grid, dim3 block,
                        hipStream_t st) {
-  if (grp <= 4) launch_split<NT, 1>(a, norm, debug, grid, block, st);
-  else launch_split<NT, 2>(a, norm, debug, grid, block, st);
+  if (grp <= 4) launch_split<NT, 1, BPS>(a, norm, debug, grid, block, st);
+  else launch_split<NT, 2, BPS>(a, norm, debug, grid, block, st);
+}
+
+template <int NT>
+void launch_split_run(const DecodeArgs& a, int grp, int norm, bool debug, dim3 grid, dim3 block,
+                      hipStream_t st) {
+  switch (a.bps) {
+    case 8: launch_split_rows<NT, 8>(a, grp, norm, debug, grid, block, st); break;
+    case 4: launch_split_rows<NT, 4>(a, grp, norm, debug, grid, block, st); break;
+    default: launch_split_rows<NT, 2>(a, grp, norm, debug, grid, block, st); break;
+  }
+}
+
+template <int G>
+void launch_scores(const DecodeArgs& a, int run, dim3 block, hipStream_t st) {
+  const int head_groups = (a.hkv + a.waves - 1) / a.waves;
+  const dim3 grid(head_groups, (a.NB + run - 1) / run, a.batch);
+  switch (run) {
+    case 8: k_decode_scores<G, 8><<<grid, block, 0, st>>>(a); break;
+    case 2: k_decode_scores<G, 2><<<grid, block, 0, st>>>(a); break;
+    default: k_decode_scores<G, 1><<<grid, block, 0, st>>>(a); break;
+  }
 }
 
 }  // namespace
 
-size_t decode_workspace_bytes(int batch, int hq, int D, int NB) {
+size_t decode_workspace_bytes(int batch, int hq, int hkv, int D, int NB) {
+  const int waves = hkv < kMaxWaves ? hkv : kMaxWaves;
   size_t off[7];
-  decode_offsets(batch, hq, D, NB, off);
+  decode_offsets(batch, hq, D, NB, pick_split((hkv + waves - 1) / waves, batch, NB), off);
   return off[6];
 }
 
 hipError_t launch_decode(const DecodeLaunch& d, hipStream_t st) {
+  const int waves = d.hkv < kMaxWaves ? d.hkv : kMaxWaves;
+  const int head_groups = (d.hkv + waves - 1) / waves;
+  const int run = pick_run(head_groups, d.batch, d.NB);
+  const int bps = pick_split(head_groups, d.batch, d.NB);
   size_t off[7];
-  decode_offsets(d.batch, d.hq, d.D, d.NB, off);
+  decode_offsets(d.batch, d.hq, d.D, d.NB, bps, off);
   uint8_t* ws = d.ws;
   DecodeArgs a;
   a.qc = ws + off[0];
@@ -616,29 +691,29 @@ hipError_t launch_decode(const DecodeLaunch& d, hipStream_t st) {
   a.hq = d.hq;
   a.hkv = d.hkv;
   a.D = d.D;
-  a.n_split = (d.NB + kBlocksPerSplit - 1) / kBlocksPerSplit;
-  a.waves = d.hkv < kMaxWaves ? d.hkv : kMaxWaves;
+  a.bps = bps;
+  a.n_split = (d.NB + bps - 1) / bps;
+  a.mxs = maxima_stride(d.NB);
+  a.waves = waves;
   a.c = d.c;
   const int grp = d.hq / d.hkv;
   hipError_t e = launch_quant_rows(d.q, d.s, ws + off[0], reinterpret_cast<uint32_t*>(ws + off[1]), d.batch, d.hq,
                                    d.hkv, d.D, false, st);
   if (e != hipSuccess) return e;
   const dim3 block(64 * a.waves);
-  const int head_groups = (d.hkv + a.waves - 1) / a.waves;
-  const dim3 g1(head_groups, (d.NB + kScoreBlocksPerWave - 1) / kScoreBlocksPerWave, d.batch);
   switch (d.D) {
-    case 64: k_decode_scores<1><<<g1, block, 0, st>>>(a); break;
-    case 128: k_decode_scores<2><<<g1, block, 0, st>>>(a); break;
-    default: k_decode_scores<4><<<g1, block, 0, st>>>(a); break;
+    case 64: launch_scores<1>(a, run, block, st); break;
+    case 128: launch_scores<2>(a, run, block, st); break;
+    default: launch_scores<4>(a, run, block, st); break;
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (d.ev && (e = hipEventRecord(d.ev[1], st)) != hipSuccess) return e;
   const dim3 g2(head_groups, a.n_split, d.batch);
   const bool dbg = d.dbg_codes != nullptr;
   switch (d.D) {
-    case 64: launch_split_rows<2>(a, grp, d.norm, dbg, g2, block, st); break;
-    case 128: launch_split_rows<4>(a, grp, d.norm, dbg, g2, block, st); break;
-    default: launch_split_rows<8>(a, grp, d.norm, dbg, g2, block, st); break;
+    case 64: launch_split_run<2>(a, grp, d.norm, dbg, g2, block, st); break;
+    case 128: launch_split_run<4>(a, grp, d.norm, dbg, g2, block, st); break;
+    default: launch_split_run<8>(a, grp, d.norm, dbg, g2, block, st); break;
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const int parts = kMergeThreads / d.D;

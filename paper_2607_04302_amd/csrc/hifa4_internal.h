@@ -85,7 +85,7 @@ struct DecodeLaunch {
   float c;
 };
 
-size_t decode_workspace_bytes(int batch, int hq, int D, int NB);
+size_t decode_workspace_bytes(int batch, int hq, int hkv, int D, int NB);
 hipError_t launch_decode(const DecodeLaunch& d, hipStream_t st);
 
 hipError_t launch_quant_rows(const half_t* x, const float* s, uint8_t* codes, uint32_t* meta, long n_rows,

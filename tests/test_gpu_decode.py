@@ -93,6 +93,7 @@ def _last_queries(q, cu):
     (128, 6, 2, (150, 700), 4, True),                 # GQA x3 (one wave idle)
     (128, 4, 1, (0, 300, 0, 65), 7, True),            # empty sequences (their rows are left untouched)
     (64, 24, 12, (100, 37), 8, True),                 # 12 kv heads: two workgroups per key range
+    (128, 16, 2, (1000, 77), 14, True),               # GQA x8 at D=128
 ])
 def test_decode_varlen_parity(h, d, hq, hkv, lens, seed, smooth):
     q, k, v, cu = small_case(heads_q=hq, heads_kv=hkv, head_dim=d, seqlens=lens, seed=seed)
@@ -113,14 +114,19 @@ def test_decode_fixed_length(h):
     _decode_and_compare(h, qd, k4, v4, None, None, 130)
 
 
-@pytest.mark.parametrize("length,d,hq,seed", [(5000, 128, 4, 5), (33000, 64, 2, 6)])
-def test_decode_many_splits(h, length, d, hq, seed):
-    """Long single sequences: 79 blocks in 10 splits, and 516 blocks in 65
-    splits (more than one 64-split pass of the merge)."""
-    q, k, v, cu = small_case(heads_q=hq, heads_kv=1, head_dim=d, seqlens=(length,), seed=seed)
-    s = np.exp(np.random.default_rng(seed).uniform(-1, 1, (1, d))).astype(np.float32)
-    _say("decode long", length)
-    _decode_and_compare(h, _last_queries(q, cu), k, v, cu, s, length)
+@pytest.mark.parametrize("lens,d,hq,hkv,seed", [
+    ((5000,), 128, 4, 1, 5),          # 79 blocks: score runs of 1, 40 splits of 2
+    ((19000,), 128, 4, 1, 12),        # 297 blocks: 75 splits of 4
+    ((33000,), 64, 2, 1, 6),          # 516 blocks: 65 splits of 8 (two 64-split passes of the merge)
+    ((16384, 16384), 64, 16, 16, 13), # two workgroups of kv heads: score runs of 2, 64 splits of 4
+])
+def test_decode_many_splits(h, lens, d, hq, hkv, seed):
+    """Long sequences, one shape per score-run and split length the launch
+    picks from the block count, batch and kv heads."""
+    q, k, v, cu = small_case(heads_q=hq, heads_kv=hkv, head_dim=d, seqlens=lens, seed=seed)
+    s = np.exp(np.random.default_rng(seed).uniform(-1, 1, (hkv, d))).astype(np.float32)
+    _say("decode long", lens, d, hq, hkv)
+    _decode_and_compare(h, _last_queries(q, cu), k, v, cu, s, max(lens))
 
 
 def test_decode_cache_append(h):
