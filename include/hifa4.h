@@ -74,7 +74,9 @@ typedef enum {
  * lengths and key j is visible to query i iff j <= i.
  *   head_dim     in {64, 128, 256};
  *   max_seqlen   fixed length (BSHD) or, with cu_seqlens, an upper bound of
- *                every sequence length (host value);
+ *                every sequence length (host value; a longer sequence is
+ *                outside the contract: the kernels clamp its length to
+ *                max_seqlen, so no access leaves the buffers);
  *   cu_seqlens   NULL for BSHD, else a DEVICE int32 array [batch+1] of
  *                non-decreasing prefix sums starting at 0 (THD layout);
  *   total_tokens with cu_seqlens: cu_seqlens[batch] (host value); ignored

@@ -13,6 +13,7 @@
 #include <string>
 #include <vector>
 
+#include "hifa4_decode.h"
 #include "hifa4_internal.h"
 
 namespace {

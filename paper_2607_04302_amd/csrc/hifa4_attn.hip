@@ -55,7 +55,7 @@ __device__ __forceinline__ TileMap map_tile(const AttnArgs& a, int heads_per_wg,
   m.hk = m.hq / (a.hq / a.hkv);
   const int span = 32 * qsub;
   m.t0 = a.cu ? a.cu[m.b] : m.b * a.S;
-  m.L = a.cu ? a.cu[m.b + 1] - m.t0 : a.S;
+  m.L = a.cu ? min(a.cu[m.b + 1] - m.t0, a.S) : a.S;     // lengths above max_seqlen are clamped (outside the contract)
   const int q0 = qt * span;
   m.wg_live = q0 < m.L;
   m.qw = q0 + 32 * (wave % qsub);

@@ -44,6 +44,7 @@
 // Workgroups hold one wave per kv head (up to eight): the heads of a token
 // share cache lines, so the lines are read once by one compute unit.
 #include "hifa4_device.h"
+#include "hifa4_decode.h"
 #include "hifa4_internal.h"
 #include "hifa4_packed.h"
 
@@ -68,7 +69,9 @@ constexpr int kMaxSplitsPerRow = 128;
 constexpr int kMaxWaves = 8;             // kv heads per workgroup
 
 __device__ __forceinline__ int dseq_start(const int* cu, int b, int S) { return cu ? cu[b] : b * S; }
-__device__ __forceinline__ int dseq_len(const int* cu, int b, int S) { return cu ? cu[b + 1] - cu[b] : S; }
+// a length above max_seqlen is outside the contract; clamping it keeps every
+// access inside the caller's buffers
+__device__ __forceinline__ int dseq_len(const int* cu, int b, int S) { return cu ? min(cu[b + 1] - cu[b], S) : S; }
 
 __device__ __forceinline__ half_t exp2_h(half_t x) { return exp2_h2(h2_t{x, (half_t)0})[0]; }
 __device__ __forceinline__ half_t hmax(half_t a, half_t b) { return a > b ? a : b; }

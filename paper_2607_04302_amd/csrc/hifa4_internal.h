@@ -66,28 +66,6 @@ struct AttnArgs {
   float c;                 // log2(e)/sqrt(D)
 };
 
-// One decode step over a packed HIF4 cache (one query row per sequence).
-struct DecodeLaunch {
-  const half_t* q;         // [batch, Hq, D] fp16
-  const float* s;          // smoothing scales or nullptr
-  const int* cu;           // cu_seqlens of the cached tokens or nullptr
-  const uint8_t* kc;       // canonical K^ cache [tokens, Hkv, D/64, 32]
-  const uint32_t* km;
-  const uint8_t* vc;       // canonical V^ cache [batch, NB, Hkv, D, 32]
-  const uint32_t* vm;
-  half_t* o;               // [batch, Hq, D]
-  float* lse;              // [Hq, batch]
-  uint8_t* dbg_codes;      // optional P^ dump [Hq, batch, NB, 32]
-  uint32_t* dbg_meta;
-  uint8_t* ws;
-  hipEvent_t* ev;          // optional; ev[1] is recorded after the score kernel
-  int batch, S, NB, hq, hkv, D, norm;
-  float c;
-};
-
-size_t decode_workspace_bytes(int batch, int hq, int hkv, int D, int NB);
-hipError_t launch_decode(const DecodeLaunch& d, hipStream_t st);
-
 hipError_t launch_quant_rows(const half_t* x, const float* s, uint8_t* codes, uint32_t* meta, long n_rows,
                              int heads, int heads_kv, int D, bool is_k, hipStream_t st);
 hipError_t launch_quant_v(const half_t* v, const int* cu, uint8_t* codes, uint32_t* meta, int batch, int S, int NB,

@@ -14,8 +14,10 @@ namespace hifa4 {
 __device__ __forceinline__ int seq_start(const int* cu, int b, int S) {
   return cu ? cu[b] : b * S;
 }
+// a length above max_seqlen is outside the contract; clamping it keeps every
+// access inside the caller's buffers
 __device__ __forceinline__ int seq_len(const int* cu, int b, int S) {
-  return cu ? cu[b + 1] - cu[b] : S;
+  return cu ? min(cu[b + 1] - cu[b], S) : S;
 }
 
 // Load 32 consecutive fp16 channels of one (token, head) row and apply the
