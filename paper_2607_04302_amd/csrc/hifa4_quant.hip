@@ -295,16 +295,25 @@ __global__ void __launch_bounds__(512) k_prep_kv_hif4(const half_t* __restrict__
     if (h == 0)
       reinterpret_cast<uint32_t*>(chunk + lay.k_scale)[(t * G + g) * 32 + (lane & 31)] = split_scale_word(go.base);
   } else {
-    // stage V rows [64J, 64J+64) of this head, zero past the sequence end
+    // stage V rows [64J, 64J+64) of this head, zero past the sequence end:
+    // 64 * D / 8 pieces of 16 bytes, 4 per thread, all loads issued before
+    // the first store (rows past the end load the last row, then store zero)
     half_t* vt = reinterpret_cast<half_t*>(sm);        // [64 keys][D]
-    const int n16 = 64 * D / 8;
-    for (int i = threadIdx.x; i < n16; i += blockDim.x) {
-      const int key = i / (D / 8), c8 = i % (D / 8);
-      const int pos = 64 * J + key;
-      uint4 val = make_uint4(0, 0, 0, 0);
-      if (pos < L) val = *reinterpret_cast<const uint4*>(v + ((size_t)(t0 + pos) * heads_kv + hk) * D + 8 * c8);
-      reinterpret_cast<uint4*>(vt)[i] = val;
+    const int pieces_per_row = D / 8;
+    uint4 val[4];
+    bool live[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int i = threadIdx.x + r * blockDim.x;
+      const int pos = 64 * J + i / pieces_per_row;
+      live[r] = pos < L;
+      const int row = live[r] ? pos : L - 1;             // L > 64 J >= 0 here
+      val[r] = *reinterpret_cast<const uint4*>(v + ((size_t)(t0 + row) * heads_kv + hk) * D +
+                                               8 * (i % pieces_per_row));
     }
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      reinterpret_cast<uint4*>(vt)[threadIdx.x + r * blockDim.x] = live[r] ? val[r] : make_uint4(0, 0, 0, 0);
     __syncthreads();
     const int dt = wave;
     const int d = 32 * dt + (lane & 31);
