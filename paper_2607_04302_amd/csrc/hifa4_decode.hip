@@ -128,8 +128,8 @@ __device__ __forceinline__ i16_t group_dot(i4_t a0, i4_t a1, uint4 w, uint32_t m
 }
 
 struct DecodeArgs {
-  const uint8_t* qc;       // canonical Q^ of the decode rows [batch, Hq, G, 32]
-  const uint32_t* qm;      // [batch, Hq, G]
+  const half_t* q;         // raw decode queries [batch, Hq, D] fp16
+  const float* s;          // smoothing scales [Hkv, D] or null
   const uint8_t* kc;       // canonical K^ cache [tokens, Hkv, G, 32]
   const uint32_t* km;      // [tokens, Hkv, G]
   const uint8_t* vc;       // canonical V^ cache [batch, NB, Hkv, D, 32]
@@ -165,6 +165,8 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (G <= 2 ? 4 : 2)) k_decode_sco
   constexpr int kScoreBlocksPerWave = RUN;
   __shared__ __align__(16) half_t lds_s[kMaxWaves][8][kScoreBlocksPerWave * 64];
   __shared__ half_t lds_m[kMaxWaves][8][kScoreBlocksPerWave];
+  __shared__ __align__(16) int8_t lds_q[kMaxWaves][8 * G * 64];   // A operands [row][group][64]
+  __shared__ uint32_t lds_qb[kMaxWaves][8 * G];                    // their bases
   const int wave = (int)(threadIdx.x >> 6);
   const int hk = blockIdx.x * a.waves + wave;
   if (hk >= a.hkv) return;
@@ -195,33 +197,83 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (G <= 2 ? 4 : 2)) k_decode_sco
       }
     }
   };
-  // the query rows: codes of row n, weights of the output rows 4h + c
-  const int qr = n < grp ? n : 0;
-  uint4 qw4[G];
-  uint32_t qmeta[G];
+  // Q^ of the group's query rows, quantized here (each workgroup of the
+  // sequence repeats it: a few hundred instructions against a separate
+  // launch).  Pass p: lane i takes (row, group) pair 4p + (i >> 4) and its
+  // channels 4(i & 15)..+3, one E3 block; q~ = fp16(fp32(q) * s).  Every load
+  // of every pass is issued first (rows past the group read row 0).
+  constexpr int D = 64 * G;
+  constexpr int kQPasses = 2 * G;                           // 8 rows x G groups / 4 per pass
+  const int kq = lane & 15;
+  uint2 qraw[kQPasses];
+  float4 qs[kQPasses];
 #pragma unroll
-  for (int g = 0; g < G; ++g) {
-    const size_t qi = (row0 + qr) * G + g;
-    qw4[g] = *reinterpret_cast<const uint4*>(a.qc + qi * 32 + 16 * h);
-    qmeta[g] = a.qm[qi];
+  for (int p = 0; p < kQPasses; ++p) {
+    const int pi = 4 * p + (lane >> 4), r = pi / G, g = pi % G;
+    const int ch = 64 * g + 4 * kq;
+    qraw[p] = *reinterpret_cast<const uint2*>(a.q + (row0 + (r < grp ? r : 0)) * D + ch);
+    qs[p] = a.s ? *reinterpret_cast<const float4*>(a.s + (size_t)hk * D + ch) : make_float4(1.0f, 1.0f, 1.0f, 1.0f);
   }
   // every prefetch is unconditional (past the run's end it reloads the last
   // block), so the number of loads in flight is the same on every path
   KBlock b0, b1;
   load(J0, b0);
+  // HIF4 of each group (the row base over 16 lanes, E2 over a lane pair, E3
+  // in-lane), the int8 operand values 4u 2^-sh with their signs written to
+  // LDS in the A-operand layout, the bases beside them
+  int8_t* lq = lds_q[wave];
+#pragma unroll
+  for (int p = 0; p < kQPasses; ++p) {
+    const int pi = 4 * p + (lane >> 4), r = pi / G, g = pi % G;
+    if (4 * p >= grp * G) break;                             // uniform: no pair of this pass is live
+    const h2_t x01 = __builtin_bit_cast(h2_t, qraw[p].x), x23 = __builtin_bit_cast(h2_t, qraw[p].y);
+    const float sv[4] = {qs[p].x, qs[p].y, qs[p].z, qs[p].w};
+    const half_t xin[4] = {x01[0], x01[1], x23[0], x23[1]};
+    float ax[4];
+    bool neg[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const half_t xs = (half_t)((float)xin[j] * sv[j]);
+      ax[j] = fabsf((float)xs);
+      neg[j] = (float)xs < 0.0f;
+    }
+    const float a4 = fmaxf(fmaxf(ax[0], ax[1]), fmaxf(ax[2], ax[3]));
+    const float a8 = fmaxf(a4, __shfl_xor(a4, 1));
+    float A = a8;
+#pragma unroll
+    for (int o = 2; o < 16; o <<= 1) A = fmaxf(A, __shfl_xor(A, o));
+    const uint32_t base = e6m2_ceil(A);
+    const float bval = e6m2_value(base);
+    const bool e2 = a8 <= 0.875f * bval;
+    const bool e3 = a4 <= (e2 ? 0.4375f : 0.875f) * bval;
+    const int sh = (int)e2 + (int)e3;
+    const float R = hif4_rcp_step(base);
+    const float C = round_const(sh);
+    if (r < grp) {
+      int8_t* dst = lq + (r * G + g) * 64 + 16 * (kq >> 2);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int u = (int)(__float_as_uint(__builtin_fmaf(ax[j], R, C)) - __float_as_uint(C));
+        const int v = u << (2 - sh);
+        dst[operand_byte(4 * (kq & 3) + j)] = (int8_t)(neg[j] ? -v : v);
+      }
+      if (kq == 0) lds_qb[wave][r * G + g] = base;
+    }
+  }
+  // A operands of row n (zero past the group), weights of the output rows 4h + c
   i4_t qa[G][2];
   float wq[G][4];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
     qa[g][0] = qa[g][1] = i4_t{0, 0, 0, 0};
     if (n < grp) {
-      qa[g][0] = decode_quarter(qw4[g].x, qw4[g].y, qmeta[g], 2 * h);
-      qa[g][1] = decode_quarter(qw4[g].z, qw4[g].w, qmeta[g], 2 * h + 1);
+      qa[g][0] = *reinterpret_cast<const i4_t*>(lq + (n * G + g) * 64 + 32 * h);
+      qa[g][1] = *reinterpret_cast<const i4_t*>(lq + (n * G + g) * 64 + 32 * h + 16);
     }
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      const uint32_t mr = (uint32_t)__shfl((int)qmeta[g], 4 * h + c);
-      wq[g][c] = (0.25f * e6m2_value(mr & 255u)) * a.c;
+      const int r = 4 * h + c;
+      wq[g][c] = (0.25f * e6m2_value(lds_qb[wave][(r < grp ? r : 0) * G + g])) * a.c;
     }
   }
   load(min(J0 + 1, J1 - 1), b1);
@@ -596,17 +648,14 @@ int pick_split(int head_groups, int batch, int NB) {
 
 int maxima_stride(int NB) { return (NB + 7) & ~7; }
 
-void decode_offsets(int batch, int hq, int D, int NB, int bps, size_t off[7]) {
-  const int G = D / 64;
+void decode_offsets(int batch, int hq, int D, int NB, int bps, size_t off[5]) {
   const int n_split = (NB + bps - 1) / bps;
   size_t o = 0;
-  off[0] = o; o += round_up256((size_t)batch * hq * G * 32);                 // Q^ codes
-  off[1] = o; o += round_up256((size_t)batch * hq * G * 4);                  // Q^ metadata
-  off[2] = o; o += round_up256((size_t)batch * hq * NB * 64 * 2);            // scores
-  off[3] = o; o += round_up256((size_t)batch * hq * maxima_stride(NB) * 2);  // block maxima
-  off[4] = o; o += round_up256((size_t)batch * hq * n_split * D * 4);        // partial O
-  off[5] = o; o += round_up256((size_t)batch * hq * n_split * 16);           // l, factor product, max
-  off[6] = o;
+  off[0] = o; o += round_up256((size_t)batch * hq * NB * 64 * 2);            // scores
+  off[1] = o; o += round_up256((size_t)batch * hq * maxima_stride(NB) * 2);  // block maxima
+  off[2] = o; o += round_up256((size_t)batch * hq * n_split * D * 4);        // partial O
+  off[3] = o; o += round_up256((size_t)batch * hq * n_split * 16);           // l, factor product, max
+  off[4] = o;
 }
 
 template <typename K>
@@ -659,9 +708,9 @@ void launch_scores(const DecodeArgs& a, int run, dim3 block, hipStream_t st) {
 
 size_t decode_workspace_bytes(int batch, int hq, int hkv, int D, int NB) {
   const int waves = hkv < kMaxWaves ? hkv : kMaxWaves;
-  size_t off[7];
+  size_t off[5];
   decode_offsets(batch, hq, D, NB, pick_split((hkv + waves - 1) / waves, batch, NB), off);
-  return off[6];
+  return off[4];
 }
 
 hipError_t launch_decode(const DecodeLaunch& d, hipStream_t st) {
@@ -669,21 +718,21 @@ hipError_t launch_decode(const DecodeLaunch& d, hipStream_t st) {
   const int head_groups = (d.hkv + waves - 1) / waves;
   const int run = pick_run(head_groups, d.batch, d.NB);
   const int bps = pick_split(head_groups, d.batch, d.NB);
-  size_t off[7];
+  size_t off[5];
   decode_offsets(d.batch, d.hq, d.D, d.NB, bps, off);
   uint8_t* ws = d.ws;
   DecodeArgs a;
-  a.qc = ws + off[0];
-  a.qm = reinterpret_cast<const uint32_t*>(ws + off[1]);
+  a.q = d.q;
+  a.s = d.s;
   a.kc = d.kc;
   a.km = d.km;
   a.vc = d.vc;
   a.vm = d.vm;
   a.cu = d.cu;
-  a.s2 = reinterpret_cast<half_t*>(ws + off[2]);
-  a.mx = reinterpret_cast<half_t*>(ws + off[3]);
-  a.opart = reinterpret_cast<float*>(ws + off[4]);
-  a.spart = reinterpret_cast<float4*>(ws + off[5]);
+  a.s2 = reinterpret_cast<half_t*>(ws + off[0]);
+  a.mx = reinterpret_cast<half_t*>(ws + off[1]);
+  a.opart = reinterpret_cast<float*>(ws + off[2]);
+  a.spart = reinterpret_cast<float4*>(ws + off[3]);
   a.o = d.o;
   a.lse = d.lse;
   a.dbg_codes = d.dbg_codes;
@@ -700,9 +749,7 @@ hipError_t launch_decode(const DecodeLaunch& d, hipStream_t st) {
   a.waves = waves;
   a.c = d.c;
   const int grp = d.hq / d.hkv;
-  hipError_t e = launch_quant_rows(d.q, d.s, ws + off[0], reinterpret_cast<uint32_t*>(ws + off[1]), d.batch, d.hq,
-                                   d.hkv, d.D, false, st);
-  if (e != hipSuccess) return e;
+  hipError_t e;
   const dim3 block(64 * a.waves);
   switch (d.D) {
     case 64: launch_scores<1>(a, run, block, st); break;

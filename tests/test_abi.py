@@ -104,24 +104,23 @@ def test_decode_validation_codes(lib):
 
 
 def test_decode_workspace_sizes(lib):
-    # B=2, Hq=32, D=128, S=4096: Q^ 2*32*2*32 B + meta 2*32*2*4 B (each
-    # rounded to 256 B), scores 2*32*64*64*2 B, block maxima 2*32*64*2 B, and
+    # B=2, Hq=32, D=128, S=4096: scores 2*32*64*64*2 B, block maxima 2*32*64*2 B, and
     # per row and split partial O (128 fp32) and (l, factor product, max).
     # Splits of 8 or 4 blocks would leave 16 or 32 workgroups: this shape takes
     # the shortest splits, 2 blocks (32 per row).
     p = _p(batch=2, max_seqlen=4096, num_heads_q=32, num_heads_kv=8)
     rows = 2 * 32
-    want = 4096 + 512 + rows * 64 * 64 * 2 + rows * 64 * 2 + rows * 32 * 128 * 4 + rows * 32 * 16
+    want = rows * 64 * 64 * 2 + rows * 64 * 2 + rows * 32 * 128 * 4 + rows * 32 * 16
     assert lib.hifa4_decode_workspace_bytes(ctypes.byref(p)) == want
-    # 8 sequences of 32768 tokens keep splits of 8 blocks (512 workgroups);
     # 100 tokens (2 blocks) pad the block maxima of a row to 8 entries
     p = _p(batch=3, max_seqlen=100, num_heads_q=4, num_heads_kv=1)
     rows = 3 * 4
-    want = 768 + 256 + 256 * ((rows * 2 * 64 * 2 + 255) // 256) + 256 + 256 * ((rows * 1 * 128 * 4 + 255) // 256) + 256
+    want = 256 * ((rows * 2 * 64 * 2 + 255) // 256) + 256 + 256 * ((rows * 1 * 128 * 4 + 255) // 256) + 256
     assert lib.hifa4_decode_workspace_bytes(ctypes.byref(p)) == want
+    # 8 sequences of 32768 tokens keep splits of 8 blocks (512 workgroups)
     p = _p(batch=8, max_seqlen=32768, num_heads_q=32, num_heads_kv=8)
     rows = 8 * 32
-    want = 16384 + 2048 + rows * 512 * 64 * 2 + rows * 512 * 2 + rows * 64 * 128 * 4 + rows * 64 * 16
+    want = rows * 512 * 64 * 2 + rows * 512 * 2 + rows * 64 * 128 * 4 + rows * 64 * 16
     assert lib.hifa4_decode_workspace_bytes(ctypes.byref(p)) == want
     assert lib.hifa4_decode_workspace_bytes(ctypes.byref(_p(head_dim=80))) == 0
 
