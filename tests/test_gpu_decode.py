@@ -15,6 +15,7 @@ from oracle import attention as oatt
 from oracle import smooth as osmooth
 from paper_2607_04302_amd.workloads import WORKLOADS, make_calibration, make_decode_inputs, small_case
 
+from _edge import edge_rows
 from _gpu_util import check_close, to_gpu, to_np
 
 pytestmark = pytest.mark.gpu
@@ -104,39 +105,6 @@ def test_decode_varlen_parity(h, d, hq, hkv, lens, seed, smooth):
         _decode_and_compare(h, qd, k, v, cu, s, max(lens), norm=norm)
 
 
-def _edge_queries(b_all, hq, d, seed):
-    """Decode queries whose 64-channel groups exercise every branch of the
-    query quantizer: all zeros (base byte 0), one non-zero element, exact
-    ties of the element rounding (base 1, step 1/4: 0.125, 0.375, 0.625 round
-    away from zero), fp16 subnormals, large magnitudes, nested E2/E3 blocks,
-    and negative zeros."""
-    rng = np.random.default_rng(seed)
-    q = rng.standard_normal((b_all, hq, d)).astype(np.float16)
-    g = q.reshape(b_all, hq, d // 64, 64)
-    for i in range(g.shape[0] * g.shape[1] * g.shape[2]):
-        b, hh, gg = np.unravel_index(i, g.shape[:3])
-        kind = i % 7
-        x = g[b, hh, gg]
-        if kind == 0:
-            x[:] = 0
-        elif kind == 1:
-            x[:] = 0
-            x[rng.integers(64)] = -3.0
-        elif kind == 2:
-            x[:] = np.tile(np.array([1.75, 0.125, -0.375, 0.625], np.float16), 16)
-        elif kind == 3:
-            x[:] = (rng.integers(-40, 41, 64) * 2.0 ** -24).astype(np.float16)
-        elif kind == 4:
-            x[:] = (rng.standard_normal(64) * 150).astype(np.float16)
-        elif kind == 5:
-            x[:] = (rng.standard_normal(64) * 0.01).astype(np.float16)
-            x[3] = 1.0
-            x[12:16] = 0.3
-        else:
-            x[::2] = np.float16(-0.0)
-    return q
-
-
 @pytest.mark.parametrize("d,hq,hkv,smooth", [(128, 8, 2, False), (128, 8, 2, True), (64, 6, 2, False),
                                              (256, 8, 1, True)])
 def test_decode_query_edge_values(h, d, hq, hkv, smooth):
@@ -146,7 +114,7 @@ def test_decode_query_edge_values(h, d, hq, hkv, smooth):
     lens = (300, 77)
     _, k, v, cu = small_case(heads_q=hq, heads_kv=hkv, head_dim=d, seqlens=lens, seed=21)
     s = np.exp(np.random.default_rng(21).uniform(-1, 1, (hkv, d))).astype(np.float32) if smooth else None
-    qd = _edge_queries(len(lens), hq, d, 22)
+    qd = edge_rows(np.random.default_rng(22).standard_normal((len(lens), hq, d)).astype(np.float16), 22)
     _say("decode edge queries", d, hq, hkv, smooth)
     _decode_and_compare(h, qd, k, v, cu, s, max(lens))
 

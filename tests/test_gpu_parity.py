@@ -14,6 +14,7 @@ from oracle import smooth as osmooth
 from oracle.softmax16 import exp2_fp16
 from paper_2607_04302_amd.workloads import WORKLOADS, make_calibration, make_inputs, small_case
 
+from _edge import edge_rows, edge_tokens
 from _gpu_util import check_close, to_gpu, to_np
 
 pytestmark = pytest.mark.gpu
@@ -54,6 +55,33 @@ def test_quantize_qk_bitexact(h, d, hq, hkv, lens):
         assert np.array_equal(to_np(g[1]).view(np.uint32), qm)
         assert np.array_equal(to_np(g[2]), kc)
         assert np.array_equal(to_np(g[3]).view(np.uint32), km)
+
+
+@pytest.mark.parametrize("d", [64, 128, 256])
+def test_quantize_edge_values_bitexact(h, d):
+    """Q^, K^ and V^ codes and metadata of inputs built from the quantizer's
+    special cases (zero groups, one element, rounding ties, subnormals, large
+    magnitudes, nested E2/E3 blocks, negative zeros), with and without
+    smoothing."""
+    lens = (130, 64, 1, 77)
+    q, k, v, cu = small_case(heads_q=4, heads_kv=2, head_dim=d, seqlens=lens, seed=31)
+    edge_rows(q, 31)
+    edge_rows(k, 32)
+    edge_tokens(v, cu, 33)
+    s = np.exp(np.random.default_rng(34).uniform(-2, 2, (2, d))).astype(np.float32)
+    for sv in (None, s):
+        qc, qm, kc, km = oatt.quantize_qk(q, k, sv)
+        g = h.hifa4_quantize_qk(to_gpu(q), to_gpu(k), None if sv is None else to_gpu(sv),
+                                cu_seqlens=to_gpu(cu), max_seqlen=max(lens))
+        assert np.array_equal(to_np(g[0]), qc)
+        assert np.array_equal(to_np(g[1]).view(np.uint32), qm)
+        assert np.array_equal(to_np(g[2]), kc)
+        assert np.array_equal(to_np(g[3]).view(np.uint32), km)
+    nb = -(-max(lens) // 64)
+    gv = h.hifa4_quantize_v(to_gpu(v), cu_seqlens=to_gpu(cu), max_seqlen=max(lens))
+    codes, meta = _canon_v_padded(v, cu, nb)
+    assert np.array_equal(to_np(gv[0]), codes)
+    assert np.array_equal(to_np(gv[1]).view(np.uint32), meta)
 
 
 def _canon_v_padded(v, cu, nb):
@@ -151,6 +179,22 @@ def test_varlen_parity(h, d, hq, hkv, lens, seed):
     _say("varlen", d, hq, hkv, lens)
     _run_and_compare(h, q, k, v, cu, s, max(lens))
     _run_and_compare(h, q, k, v, cu, None, max(lens), norm="inconsistent")
+
+
+@pytest.mark.parametrize("d,hq,hkv,smooth", [(128, 4, 2, False), (64, 2, 1, True), (256, 2, 1, False)])
+def test_edge_values_parity(h, d, hq, hkv, smooth):
+    """The attention kernel's own quantizers (Q in its prologue, K and V in
+    the pre-pass) on inputs built from the quantizer's special cases: every
+    P^ code bit-exact, O and LSE within tolerance.  Magnitudes stay below 40
+    so that no score leaves the fp16 range."""
+    lens = (200, 77)
+    q, k, v, cu = small_case(heads_q=hq, heads_kv=hkv, head_dim=d, seqlens=lens, seed=41)
+    edge_rows(q, 41, large=40.0)
+    edge_rows(k, 42, large=40.0)
+    edge_tokens(v, cu, 43, large=40.0)
+    s = np.exp(np.random.default_rng(44).uniform(-1, 1, (hkv, d))).astype(np.float32) if smooth else None
+    _say("edge values", d, hq, hkv, smooth)
+    _run_and_compare(h, q, k, v, cu, s, max(lens))
 
 
 def test_fp16_variant(h):
