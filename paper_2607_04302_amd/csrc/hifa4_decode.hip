@@ -11,8 +11,9 @@
 // range is split; the split must not change any P^ code, because P^ depends
 // on the running maximum entering each 64-key block.  Three kernels keep every
 // decision of the sequential loop:
-//   1. scores: per (sequence, run of 64-key blocks, kv head) the fp16 scores
-//      S2 of the GQA group's query rows, stored, and each row's block maximum;
+//   1. scores: per (sequence, run of 64-key blocks, kv head) the query rows
+//      of the GQA group are smoothed and quantized (Q^ = HIF4(fp16(q s))),
+//      then the fp16 scores S2 are stored with each row's block maximum;
 //   2. splits: each wave takes a run of blocks and starts from the running
 //      maximum the sequential loop has at its first block (the prefix maximum
 //      of the stored block maxima), then applies the FP16 softmax,
@@ -39,7 +40,8 @@
 // contiguous code bytes.  Only the pairing of k indices between A and B
 // matters for a dot product, and both operands place a quarter's sixteen
 // elements in the same (decode) order.  The output lane l holds column
-// (l & 31) and, in its first four values, rows 4h + c.
+// (l & 31) and, in its first four values, rows 4h + c, so a wave serves at
+// most eight query rows: GQA groups of up to 8 heads per kv head.
 //
 // Workgroups hold one wave per kv head (up to eight): the heads of a token
 // share cache lines, so the lines are read once by one compute unit.
