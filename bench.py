@@ -219,9 +219,9 @@ def decode_report(h, torch, np, ws, steps=50):
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) * 1e3 / steps
     dev_ms = da.elapsed_time(db) / steps
-    # the split between the score kernel and the split kernel plus merge, from
-    # the library's events inside each call (a separate pass: those events
-    # add their own gaps)
+    # the split between scores plus splits and the merge, from the library's
+    # events inside each call (a separate pass: those events add their own
+    # gaps)
     for i in range(steps):
         h.hifa4_decode_fwd(q, kcode, kmeta, vcode, vmeta, s, timing_events=evs[i], **kw)
     torch.cuda.synchronize()
@@ -254,7 +254,7 @@ def decode_report(h, torch, np, ws, steps=50):
            "cache_bytes": cache, "fp16_cache_bytes": 2 * 2 * w.total_tokens() * w.heads_kv * w.head_dim,
            "steps": steps, "ms_per_step": round(dev_ms, 4), "wall_ms_per_step": round(wall, 4),
            "graph_replay_ms_per_step": round(graph_ms, 4),
-           "kernels_ms": {"q_quant_and_scores": round(first, 4), "splits_and_merge": round(second, 4),
+           "kernels_ms": {"scores_and_splits": round(first, 4), "merge": round(second, 4),
                           "basis": "library events inside each call, a separate pass"},
            "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                         "frac": round(gbs / PEAK_HBM_GBS, 4),

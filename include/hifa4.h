@@ -271,9 +271,8 @@ size_t hifa4_decode_workspace_bytes(const hifa4_problem* p);
  *    [num_heads_q, batch]; rows of empty sequences are left untouched.
  * opt: norm, smooth_qk, debug_p_codes/_meta ([num_heads_q, batch, NB, 32] /
  *    [num_heads_q, batch, NB], entries J < ceil(L_b/64) written) and
- *    timing_events (before the score kernel, which also quantizes the queries,
- *    between the score kernel and the split kernel, after the merge) as for
- *    hifa4_attention_fwd; operands must be
+ *    timing_events (before the first kernel, before the merge kernel, after
+ *    the merge) as for hifa4_attention_fwd; operands must be
  *    HIFA4_OPERANDS_HIF4 and q_mean 0 (the cache carries no key sums), else
  *    HIFA4_ERR_UNSUPPORTED; num_heads_q / num_heads_kv must be <= 8 (else
  *    HIFA4_ERR_UNSUPPORTED).

@@ -19,7 +19,7 @@ struct DecodeLaunch {
   uint8_t* dbg_codes;      // optional P^ dump [Hq, batch, NB, 32]
   uint32_t* dbg_meta;
   uint8_t* ws;
-  hipEvent_t* ev;          // optional; ev[1] is recorded after the score kernel
+  hipEvent_t* ev;          // optional; ev[1] is recorded before the merge kernel
   int batch, S, NB, hq, hkv, D, norm;
   float c;
 };

@@ -45,6 +45,9 @@
 //
 // Workgroups hold one wave per kv head (up to eight): the heads of a token
 // share cache lines, so the lines are read once by one compute unit.
+#include <atomic>
+#include <random>
+
 #include "hifa4_device.h"
 #include "hifa4_decode.h"
 #include "hifa4_internal.h"
@@ -149,6 +152,42 @@ struct DecodeArgs {
   int batch, S, NB, hq, hkv, D, n_split, waves, bps;
   int mxs;                 // row stride of the block maxima: NB rounded up to 8
   float c;
+  uint64_t* runmax;        // fused path: [batch, Hq, n_split] run maxima, epoch-tagged
+  uint32_t epoch;          // fused path: this call's tag (never 0)
+};
+
+// One wave's share of a workgroup: kv head hk of sequence b, blocks
+// [J0, J1) of run (or split) `part`.
+struct WaveSpan {
+  int hk, b, L, J0, J1, t0, grp, part;
+  size_t row0;             // first query row of the GQA group
+};
+
+// False when the wave has nothing to do (no kv head, or no block in range).
+__device__ __forceinline__ bool wave_span(const DecodeArgs& a, int blocks, WaveSpan& w) {
+  w.hk = blockIdx.x * a.waves + (int)(threadIdx.x >> 6);
+  if (w.hk >= a.hkv) return false;
+  w.b = blockIdx.z;
+  w.part = blockIdx.y;
+  w.L = dseq_len(a.cu, w.b, a.S);
+  const int nblk = (w.L + 63) >> 6;
+  w.J0 = w.part * blocks;
+  if (w.J0 >= nblk) return false;
+  w.J1 = min(w.J0 + blocks, nblk);
+  w.t0 = dseq_start(a.cu, w.b, a.S);
+  w.grp = a.hq / a.hkv;
+  w.row0 = (size_t)w.b * a.hq + (size_t)w.hk * w.grp;
+  return true;
+}
+
+// LDS of the score phase, per wave: the run's scores [row][block][key], the
+// block maxima, Q^'s A operands [row][group][64] and their bases.
+template <int G, int RUN>
+struct ScoreLds {
+  half_t s[kMaxWaves][8][RUN * 64];
+  half_t m[kMaxWaves][8][RUN];
+  alignas(16) int8_t q[kMaxWaves][8 * G * 64];
+  uint32_t qb[kMaxWaves][8 * G];
 };
 
 // ---------------------------------------------------------------------------
@@ -163,25 +202,12 @@ struct DecodeArgs {
 // the run are collected in LDS and stored after the last block, so the loop
 // issues loads only.
 template <int G, int RUN>
-__global__ void __launch_bounds__(64 * kMaxWaves, (G <= 2 ? 4 : 2)) k_decode_scores(DecodeArgs a) {
+__device__ __forceinline__ void score_run(const DecodeArgs& a, const WaveSpan& w, ScoreLds<G, RUN>& sl) {
   constexpr int kScoreBlocksPerWave = RUN;
-  __shared__ __align__(16) half_t lds_s[kMaxWaves][8][kScoreBlocksPerWave * 64];
-  __shared__ half_t lds_m[kMaxWaves][8][kScoreBlocksPerWave];
-  __shared__ __align__(16) int8_t lds_q[kMaxWaves][8 * G * 64];   // A operands [row][group][64]
-  __shared__ uint32_t lds_qb[kMaxWaves][8 * G];                    // their bases
   const int wave = (int)(threadIdx.x >> 6);
-  const int hk = blockIdx.x * a.waves + wave;
-  if (hk >= a.hkv) return;
   const int lane = threadIdx.x & 63, n = lane & 31, h = lane >> 5;
-  const int b = blockIdx.z;
-  const int L = dseq_len(a.cu, b, a.S);
-  const int nblk = (L + 63) >> 6;
-  const int J0 = blockIdx.y * kScoreBlocksPerWave;
-  if (J0 >= nblk) return;
-  const int J1 = min(J0 + kScoreBlocksPerWave, nblk);
-  const int t0 = dseq_start(a.cu, b, a.S);
-  const int grp = a.hq / a.hkv;
-  const size_t row0 = (size_t)b * a.hq + (size_t)hk * grp;     // first query row of the group
+  const int hk = w.hk, L = w.L, J0 = w.J0, J1 = w.J1, t0 = w.t0, grp = w.grp;
+  const size_t row0 = w.row0;
   struct KBlock {
     uint4 w[2][G];
     uint32_t meta[2][G];
@@ -223,7 +249,7 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (G <= 2 ? 4 : 2)) k_decode_sco
   // HIF4 of each group (the row base over 16 lanes, E2 over a lane pair, E3
   // in-lane), the int8 operand values 4u 2^-sh with their signs written to
   // LDS in the A-operand layout, the bases beside them
-  int8_t* lq = lds_q[wave];
+  int8_t* lq = sl.q[wave];
 #pragma unroll
   for (int p = 0; p < kQPasses; ++p) {
     const int pi = 4 * p + (lane >> 4), r = pi / G, g = pi % G;
@@ -259,7 +285,7 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (G <= 2 ? 4 : 2)) k_decode_sco
         const int v = u << (2 - sh);
         dst[operand_byte(4 * (kq & 3) + j)] = (int8_t)(neg[j] ? -v : v);
       }
-      if (kq == 0) lds_qb[wave][r * G + g] = base;
+      if (kq == 0) sl.qb[wave][r * G + g] = base;
     }
   }
   // A operands of row n (zero past the group), weights of the output rows 4h + c
@@ -275,11 +301,11 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (G <= 2 ? 4 : 2)) k_decode_sco
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       const int r = 4 * h + c;
-      wq[g][c] = (0.25f * e6m2_value(lds_qb[wave][(r < grp ? r : 0) * G + g])) * a.c;
+      wq[g][c] = (0.25f * e6m2_value(sl.qb[wave][(r < grp ? r : 0) * G + g])) * a.c;
     }
   }
   load(min(J0 + 1, J1 - 1), b1);
-  half_t* ls = &lds_s[wave][0][0];
+  half_t* ls = &sl.s[wave][0][0];
   auto compute = [&](const KBlock& kb, int i) {
     const int J = J0 + i;
     float acc[2][4];
@@ -312,7 +338,7 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (G <= 2 ? 4 : 2)) k_decode_sco
       if (r < grp) {
         ls[r * (kScoreBlocksPerWave * 64) + 64 * i + n] = sv[0];
         ls[r * (kScoreBlocksPerWave * 64) + 64 * i + 32 + n] = sv[1];
-        if (n == 0) lds_m[wave][r][i] = (half_t)m;
+        if (n == 0) sl.m[wave][r][i] = (half_t)m;
       }
     }
   };
@@ -323,13 +349,22 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (G <= 2 ? 4 : 2)) k_decode_sco
     if (i + 1 < kScoreBlocksPerWave && J0 + i + 1 < J1) compute(b1, i + 1);
     if (i + 3 < kScoreBlocksPerWave) load(min(J0 + i + 3, J1 - 1), b1);
   }
+}
+
+template <int G, int RUN>
+__global__ void __launch_bounds__(64 * kMaxWaves, (G <= 2 ? 4 : 2)) k_decode_scores(DecodeArgs a) {
+  __shared__ __align__(16) ScoreLds<G, RUN> sl;
+  WaveSpan w;
+  if (!wave_span(a, RUN, w)) return;
+  score_run<G, RUN>(a, w, sl);
   // the run's scores (J1 - J0 blocks of 64, contiguous per row) and maxima
-  const int nb = J1 - J0;
-  for (int r = 0; r < grp; ++r) {
-    const uint2* src = reinterpret_cast<const uint2*>(ls + r * (kScoreBlocksPerWave * 64));
-    uint2* dst = reinterpret_cast<uint2*>(a.s2 + ((row0 + r) * a.NB + J0) * 64);
+  const int wave = (int)(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int nb = w.J1 - w.J0;
+  for (int r = 0; r < w.grp; ++r) {
+    const uint2* src = reinterpret_cast<const uint2*>(&sl.s[wave][r][0]);
+    uint2* dst = reinterpret_cast<uint2*>(a.s2 + ((w.row0 + r) * a.NB + w.J0) * 64);
     for (int k = lane; k < nb * 16; k += 64) dst[k] = src[k];
-    if (lane < nb) a.mx[(row0 + r) * a.mxs + J0 + lane] = lds_m[wave][r][lane];
+    if (lane < nb) a.mx[(w.row0 + r) * a.mxs + w.J0 + lane] = sl.m[wave][r][lane];
   }
 }
 
@@ -342,24 +377,17 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (G <= 2 ? 4 : 2)) k_decode_sco
 // from where lane (row l & 31, half h) reads its two operands.  B = 32
 // channels of the block's V^ groups; per 32-channel tile the two MFMAs give
 // the exact block sums, and O[row][ch] = fma(O, r_row, dot * b_V/16 * b_P/16).
-template <int NT, int RP, int NORM, bool DEBUG, int BPS>
-__global__ void __launch_bounds__(64 * kMaxWaves, (NT * RP <= 4 ? 4 : 2)) k_decode_split(DecodeArgs a) {
+// FROM_LDS: the scores and block maxima of the split's blocks are in this
+// wave's LDS (lsc [8 rows][BPS * 64], lmx [8 rows][BPS]) and m_in holds the
+// running maximum entering the split per pass; otherwise both come from HBM.
+template <int NT, int RP, int NORM, bool DEBUG, int BPS, bool FROM_LDS>
+__device__ __forceinline__ void split_run(const DecodeArgs& a, const WaveSpan& w, uint8_t* lp, const half_t* lsc,
+                                          const half_t* lmx, const half_t* m_in) {
   constexpr int kBlocksPerSplit = BPS;
   constexpr int D = 32 * NT;
-  __shared__ __align__(16) uint8_t lds_p[kMaxWaves][8 * 64];
-  const int wave = (int)(threadIdx.x >> 6);
-  const int hk = blockIdx.x * a.waves + wave;
-  if (hk >= a.hkv) return;
   const int lane = threadIdx.x & 63, n = lane & 31, h = lane >> 5;
-  const int sp = blockIdx.y, b = blockIdx.z;
-  const int L = dseq_len(a.cu, b, a.S);
-  const int nblk = (L + 63) >> 6;
-  const int J0 = sp * kBlocksPerSplit;
-  if (J0 >= nblk) return;
-  const int J1 = min(J0 + kBlocksPerSplit, nblk);
-  const int grp = a.hq / a.hkv;
-  const size_t row0 = (size_t)b * a.hq + (size_t)hk * grp;
-  uint8_t* lp = lds_p[wave];
+  const int hk = w.hk, b = w.b, sp = w.part, J0 = w.J0, J1 = w.J1, grp = w.grp;
+  const size_t row0 = w.row0;
   const int kq = lane & 15;                      // keys 4kq..4kq+3 of the block
   const int quarter = kq >> 2;                   // their group quarter
   int prow[RP];                                  // softmax row of this lane per pass
@@ -382,11 +410,13 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (NT * RP <= 4 ? 4 : 2)) k_deco
       vb.w[t] = *reinterpret_cast<const uint4*>(a.vc + gi * 32 + 16 * h);
       vb.meta[t] = a.vm[gi];
     }
+    if constexpr (!FROM_LDS) {
 #pragma unroll
-    for (int p = 0; p < RP; ++p) {
-      const size_t rj = (row0 + prow[p]) * a.NB + J;
-      vb.s[p] = *reinterpret_cast<const uint2*>(a.s2 + rj * 64 + 4 * kq);
-      vb.mx[p] = a.mx[(row0 + prow[p]) * a.mxs + J];
+      for (int p = 0; p < RP; ++p) {
+        const size_t rj = (row0 + prow[p]) * a.NB + J;
+        vb.s[p] = *reinterpret_cast<const uint2*>(a.s2 + rj * 64 + 4 * kq);
+        vb.mx[p] = a.mx[(row0 + prow[p]) * a.mxs + J];
+      }
     }
   };
   // every prefetch is unconditional (past the split's end it reloads the last
@@ -407,7 +437,7 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (NT * RP <= 4 ? 4 : 2)) k_deco
     prod[p] = 1.0f;
     pm[p] = h2_t{(half_t)(-__builtin_inff()), (half_t)(-__builtin_inff())};
   }
-  const int nch = (J0 + 7) >> 3;                 // chunks of 8 maxima before J0
+  const int nch = FROM_LDS ? 0 : (J0 + 7) >> 3;  // chunks of 8 maxima before J0
   for (int c0 = 0; c0 < nch; c0 += 16 * kPrefixLoads) {
     uint4 w[RP][kPrefixLoads];
     int nv[kPrefixLoads];
@@ -439,7 +469,7 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (NT * RP <= 4 ? 4 : 2)) k_deco
     float mm = fmaxf((float)pm[p][0], (float)pm[p][1]);
 #pragma unroll
     for (int o = 1; o < 16; o <<= 1) mm = fmaxf(mm, __shfl_xor(mm, o));
-    m[p] = (half_t)mm;
+    m[p] = FROM_LDS ? m_in[p] : (half_t)mm;
   }
   float O[NT][4];
 #pragma unroll
@@ -451,14 +481,23 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (NT * RP <= 4 ? 4 : 2)) k_deco
 #pragma unroll
     for (int p = 0; p < RP; ++p) {
       const int r = 4 * p + (lane >> 4);
+      uint2 s4;
+      half_t bmax;
+      if constexpr (FROM_LDS) {
+        s4 = *reinterpret_cast<const uint2*>(lsc + prow[p] * (BPS * 64) + 64 * (J - J0) + 4 * kq);
+        bmax = lmx[prow[p] * BPS + (J - J0)];
+      } else {
+        s4 = cur.s[p];
+        bmax = cur.mx[p];
+      }
       // FP16 softmax of the lane's four keys
-      const half_t mn = hmax(m[p], cur.mx[p]);
+      const half_t mn = hmax(m[p], bmax);
       rr[p] = (float)exp2_h(m[p] - mn);
       prod[p] *= rr[p];
       m[p] = mn;
       const h2_t mn2 = {mn, mn};
-      const h2_t p01 = exp2_h2(__builtin_bit_cast(h2_t, cur.s[p].x) - mn2);
-      const h2_t p23 = exp2_h2(__builtin_bit_cast(h2_t, cur.s[p].y) - mn2);
+      const h2_t p01 = exp2_h2(__builtin_bit_cast(h2_t, s4.x) - mn2);
+      const h2_t p23 = exp2_h2(__builtin_bit_cast(h2_t, s4.y) - mn2);
       const float ap[4] = {(float)p01[0], (float)p01[1], (float)p23[0], (float)p23[1]};
       // P^ = HIF4(P) over the row's 64 keys
       const float a4 = fmaxf(fmaxf(ap[0], ap[1]), fmaxf(ap[2], ap[3]));
@@ -560,6 +599,79 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (NT * RP <= 4 ? 4 : 2)) k_deco
   }
 }
 
+template <int NT, int RP, int NORM, bool DEBUG, int BPS>
+__global__ void __launch_bounds__(64 * kMaxWaves, (NT * RP <= 4 ? 4 : 2)) k_decode_split(DecodeArgs a) {
+  __shared__ __align__(16) uint8_t lds_p[kMaxWaves][8 * 64];
+  WaveSpan w;
+  if (!wave_span(a, BPS, w)) return;
+  split_run<NT, RP, NORM, DEBUG, BPS, false>(a, w, lds_p[threadIdx.x >> 6], nullptr, nullptr, nullptr);
+}
+
+// ---------------------------------------------------------------------------
+// 1+2. Scores and splits in one kernel, where the score runs and the splits
+// have the same length (kFusedRun blocks).  A wave computes its run's scores
+// into LDS, publishes each row's maximum over the run (tagged with the call's
+// epoch), takes the running maximum entering the run as the maximum of the
+// earlier runs' maxima of its sequence, and runs the split from LDS: the
+// scores never leave the compute unit.  The earlier runs belong to
+// workgroups with lower indices, which each XCD dispatches first, so the
+// lowest unfinished workgroup is always running; a spin limit still ends
+// every wait.
+constexpr int kFusedRun = 8;
+constexpr int kLookBatch = 4;                    // run maxima per lane per round
+constexpr int kSpinLimit = 1 << 20;
+
+template <int G, int RP, int NORM, bool DEBUG>
+__global__ void __launch_bounds__(64 * kMaxWaves, (G * RP <= 2 ? 4 : 2)) k_decode_fused(DecodeArgs a) {
+  __shared__ __align__(16) ScoreLds<G, kFusedRun> sl;
+  __shared__ __align__(16) uint8_t lds_p[kMaxWaves][8 * 64];
+  WaveSpan w;
+  if (!wave_span(a, kFusedRun, w)) return;
+  const int wave = (int)(threadIdx.x >> 6), lane = threadIdx.x & 63, kq = lane & 15;
+  score_run<G, kFusedRun>(a, w, sl);
+  const int nb = w.J1 - w.J0;
+  if (lane < w.grp) {
+    half_t rm = sl.m[wave][lane][0];
+    for (int i = 1; i < nb; ++i) rm = hmax(rm, sl.m[wave][lane][i]);
+    const uint64_t word = ((uint64_t)a.epoch << 32) | (uint64_t)__builtin_bit_cast(uint16_t, rm);
+    __hip_atomic_store(a.runmax + (w.row0 + lane) * a.n_split + w.part, word, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+  }
+  // 16 lanes per softmax row, kLookBatch run maxima each per round, every
+  // load of a round issued before the first is checked
+  half_t m_in[RP];
+#pragma unroll
+  for (int p = 0; p < RP; ++p) {
+    const int r = 4 * p + (lane >> 4);
+    const uint64_t* f = a.runmax + (w.row0 + (r < w.grp ? r : 0)) * a.n_split;
+    float mm = -__builtin_inff();
+    for (int q0 = 0; q0 < w.part; q0 += 16 * kLookBatch) {
+      uint64_t wd[kLookBatch];
+#pragma unroll
+      for (int k = 0; k < kLookBatch; ++k) {
+        const int q = q0 + 16 * k + kq;
+        wd[k] = q < w.part ? __hip_atomic_load(f + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
+      }
+#pragma unroll
+      for (int k = 0; k < kLookBatch; ++k) {
+        const int q = q0 + 16 * k + kq;
+        if (q < w.part) {
+          uint64_t v = wd[k];
+          for (int it = 0; (uint32_t)(v >> 32) != a.epoch && it < kSpinLimit; ++it) {
+            __builtin_amdgcn_s_sleep(2);
+            v = __hip_atomic_load(f + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          }
+          mm = fmaxf(mm, (float)__builtin_bit_cast(half_t, (uint16_t)v));
+        }
+      }
+    }
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) mm = fmaxf(mm, __shfl_xor(mm, o));
+    m_in[p] = (half_t)mm;
+  }
+  split_run<2 * G, RP, NORM, DEBUG, kFusedRun, true>(a, w, lds_p[wave], &sl.s[wave][0][0], &sl.m[wave][0][0], m_in);
+}
+
 // ---------------------------------------------------------------------------
 // 3. Merge.  One workgroup per row (b, query head).  Each split wrote its l,
 // the product of its blocks' rescale factors r_J = E(fp16(m_{J-1} - m_J))
@@ -650,14 +762,41 @@ int pick_split(int head_groups, int batch, int NB) {
 
 int maxima_stride(int NB) { return (NB + 7) & ~7; }
 
-void decode_offsets(int batch, int hq, int D, int NB, int bps, size_t off[5]) {
-  const int n_split = (NB + bps - 1) / bps;
+struct DecodePlan {
+  int waves, head_groups, run, bps;
+  bool fused;              // one kernel for scores and splits (run == bps == kFusedRun)
+};
+
+DecodePlan plan_decode(int batch, int hkv, int NB) {
+  DecodePlan p;
+  p.waves = hkv < kMaxWaves ? hkv : kMaxWaves;
+  p.head_groups = (hkv + p.waves - 1) / p.waves;
+  p.run = pick_run(p.head_groups, batch, NB);
+  p.bps = pick_split(p.head_groups, batch, NB);
+  p.fused = p.run == kFusedRun && p.bps == kFusedRun;
+  return p;
+}
+
+void decode_offsets(int batch, int hq, int D, int NB, const DecodePlan& pl, size_t off[6]) {
+  const size_t rows = (size_t)batch * hq;
+  const int n_split = (NB + pl.bps - 1) / pl.bps;
   size_t o = 0;
-  off[0] = o; o += round_up256((size_t)batch * hq * NB * 64 * 2);            // scores
-  off[1] = o; o += round_up256((size_t)batch * hq * maxima_stride(NB) * 2);  // block maxima
-  off[2] = o; o += round_up256((size_t)batch * hq * n_split * D * 4);        // partial O
-  off[3] = o; o += round_up256((size_t)batch * hq * n_split * 16);           // l, factor product, max
-  off[4] = o;
+  off[0] = o; o += pl.fused ? 0 : round_up256(rows * NB * 64 * 2);             // scores
+  off[1] = o; o += pl.fused ? 0 : round_up256(rows * maxima_stride(NB) * 2);   // block maxima
+  off[2] = o; o += round_up256(rows * n_split * D * 4);                         // partial O
+  off[3] = o; o += round_up256(rows * n_split * 16);                            // l, factor product, max
+  off[4] = o; o += pl.fused ? round_up256(rows * n_split * 8) : 0;              // run maxima
+  off[5] = o;
+}
+
+// Epoch tags of the fused path: a fresh value per call, starting from a
+// random point so that words another process left in reused memory do not
+// match.
+uint32_t next_epoch() {
+  static std::atomic<uint32_t> counter{(uint32_t)std::random_device{}()};
+  uint32_t e = counter.fetch_add(1) + 1;
+  if (e == 0) e = counter.fetch_add(1) + 1;
+  return e;
 }
 
 template <typename K>
@@ -695,6 +834,23 @@ void launch_split_run(const DecodeArgs& a, int grp, int norm, bool debug, dim3 g
   }
 }
 
+template <int G, int RP>
+void launch_fused_rows(const DecodeArgs& a, int norm, bool debug, dim3 grid, dim3 block, hipStream_t st) {
+  if (norm == 0) {
+    if (debug) k_decode_fused<G, RP, 0, true><<<grid, block, 0, st>>>(a);
+    else k_decode_fused<G, RP, 0, false><<<grid, block, 0, st>>>(a);
+  } else {
+    if (debug) k_decode_fused<G, RP, 1, true><<<grid, block, 0, st>>>(a);
+    else k_decode_fused<G, RP, 1, false><<<grid, block, 0, st>>>(a);
+  }
+}
+
+template <int G>
+void launch_fused(const DecodeArgs& a, int grp, int norm, bool debug, dim3 grid, dim3 block, hipStream_t st) {
+  if (grp <= 4) launch_fused_rows<G, 1>(a, norm, debug, grid, block, st);
+  else launch_fused_rows<G, 2>(a, norm, debug, grid, block, st);
+}
+
 template <int G>
 void launch_scores(const DecodeArgs& a, int run, dim3 block, hipStream_t st) {
   const int head_groups = (a.hkv + a.waves - 1) / a.waves;
@@ -709,19 +865,16 @@ void launch_scores(const DecodeArgs& a, int run, dim3 block, hipStream_t st) {
 }  // namespace
 
 size_t decode_workspace_bytes(int batch, int hq, int hkv, int D, int NB) {
-  const int waves = hkv < kMaxWaves ? hkv : kMaxWaves;
-  size_t off[5];
-  decode_offsets(batch, hq, D, NB, pick_split((hkv + waves - 1) / waves, batch, NB), off);
-  return off[4];
+  size_t off[6];
+  decode_offsets(batch, hq, D, NB, plan_decode(batch, hkv, NB), off);
+  return off[5];
 }
 
 hipError_t launch_decode(const DecodeLaunch& d, hipStream_t st) {
-  const int waves = d.hkv < kMaxWaves ? d.hkv : kMaxWaves;
-  const int head_groups = (d.hkv + waves - 1) / waves;
-  const int run = pick_run(head_groups, d.batch, d.NB);
-  const int bps = pick_split(head_groups, d.batch, d.NB);
-  size_t off[5];
-  decode_offsets(d.batch, d.hq, d.D, d.NB, bps, off);
+  const DecodePlan pl = plan_decode(d.batch, d.hkv, d.NB);
+  const int waves = pl.waves, head_groups = pl.head_groups, run = pl.run, bps = pl.bps;
+  size_t off[6];
+  decode_offsets(d.batch, d.hq, d.D, d.NB, pl, off);
   uint8_t* ws = d.ws;
   DecodeArgs a;
   a.q = d.q;
@@ -735,6 +888,8 @@ hipError_t launch_decode(const DecodeLaunch& d, hipStream_t st) {
   a.mx = reinterpret_cast<half_t*>(ws + off[1]);
   a.opart = reinterpret_cast<float*>(ws + off[2]);
   a.spart = reinterpret_cast<float4*>(ws + off[3]);
+  a.runmax = pl.fused ? reinterpret_cast<uint64_t*>(ws + off[4]) : nullptr;
+  a.epoch = pl.fused ? next_epoch() : 0;
   a.o = d.o;
   a.lse = d.lse;
   a.dbg_codes = d.dbg_codes;
@@ -753,21 +908,29 @@ hipError_t launch_decode(const DecodeLaunch& d, hipStream_t st) {
   const int grp = d.hq / d.hkv;
   hipError_t e;
   const dim3 block(64 * a.waves);
-  switch (d.D) {
-    case 64: launch_scores<1>(a, run, block, st); break;
-    case 128: launch_scores<2>(a, run, block, st); break;
-    default: launch_scores<4>(a, run, block, st); break;
+  const dim3 g2(head_groups, a.n_split, d.batch);
+  const bool dbg = d.dbg_codes != nullptr;
+  if (pl.fused) {
+    switch (d.D) {
+      case 64: launch_fused<1>(a, grp, d.norm, dbg, g2, block, st); break;
+      case 128: launch_fused<2>(a, grp, d.norm, dbg, g2, block, st); break;
+      default: launch_fused<4>(a, grp, d.norm, dbg, g2, block, st); break;
+    }
+  } else {
+    switch (d.D) {
+      case 64: launch_scores<1>(a, run, block, st); break;
+      case 128: launch_scores<2>(a, run, block, st); break;
+      default: launch_scores<4>(a, run, block, st); break;
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    switch (d.D) {
+      case 64: launch_split_run<2>(a, grp, d.norm, dbg, g2, block, st); break;
+      case 128: launch_split_run<4>(a, grp, d.norm, dbg, g2, block, st); break;
+      default: launch_split_run<8>(a, grp, d.norm, dbg, g2, block, st); break;
+    }
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (d.ev && (e = hipEventRecord(d.ev[1], st)) != hipSuccess) return e;
-  const dim3 g2(head_groups, a.n_split, d.batch);
-  const bool dbg = d.dbg_codes != nullptr;
-  switch (d.D) {
-    case 64: launch_split_run<2>(a, grp, d.norm, dbg, g2, block, st); break;
-    case 128: launch_split_run<4>(a, grp, d.norm, dbg, g2, block, st); break;
-    default: launch_split_run<8>(a, grp, d.norm, dbg, g2, block, st); break;
-  }
-  if ((e = hipGetLastError()) != hipSuccess) return e;
   const int parts = kMergeThreads / d.D;
   const size_t lds3 = ((size_t)a.n_split + (size_t)parts * d.D + parts) * sizeof(float);
   if ((e = allow_lds(k_decode_merge, lds3)) != hipSuccess) return e;

@@ -117,10 +117,12 @@ def test_decode_workspace_sizes(lib):
     rows = 3 * 4
     want = 256 * ((rows * 2 * 64 * 2 + 255) // 256) + 256 + 256 * ((rows * 1 * 128 * 4 + 255) // 256) + 256
     assert lib.hifa4_decode_workspace_bytes(ctypes.byref(p)) == want
-    # 8 sequences of 32768 tokens keep splits of 8 blocks (512 workgroups)
+    # 8 sequences of 32768 tokens: runs and splits of 8 blocks (512
+    # workgroups), one kernel for both, so no scores or block maxima, but an
+    # 8-byte run maximum per row and run
     p = _p(batch=8, max_seqlen=32768, num_heads_q=32, num_heads_kv=8)
     rows = 8 * 32
-    want = rows * 512 * 64 * 2 + rows * 512 * 2 + rows * 64 * 128 * 4 + rows * 64 * 16
+    want = rows * 64 * 128 * 4 + rows * 64 * 16 + rows * 64 * 8
     assert lib.hifa4_decode_workspace_bytes(ctypes.byref(p)) == want
     assert lib.hifa4_decode_workspace_bytes(ctypes.byref(_p(head_dim=80))) == 0
 

@@ -144,6 +144,24 @@ def test_decode_many_splits(h, lens, d, hq, hkv, seed):
     _decode_and_compare(h, _last_queries(q, cu), k, v, cu, s, max(lens))
 
 
+@pytest.mark.parametrize("lens,d,hq,hkv,seed,seqs,kv_heads", [
+    # 64 kv heads in 8 workgroups, 58 blocks: runs and splits of 8, GQA x1
+    ((3648, 3600, 3700, 3500, 3648, 3100, 3648, 3648), 64, 64, 64, 15, [0, 2, 5], [0, 37, 63]),
+    # GQA x8 (two rows per softmax lane pass), 256 blocks in 2 workgroups of kv heads
+    ((16384, 16000, 16384, 15000, 16384, 16300, 16384, 9000), 64, 128, 16, 16, [1, 7], [0, 9, 15]),
+])
+def test_decode_fused_runs(h, lens, d, hq, hkv, seed, seqs, kv_heads):
+    """Shapes where the score runs and the splits both take 8 blocks, so one
+    kernel computes the scores into LDS, publishes each row's run maximum and
+    reads the earlier runs' maxima of its sequence: every P^ code of the
+    sampled rows bit-exact."""
+    _, k, v, cu = small_case(heads_q=hkv, heads_kv=hkv, head_dim=d, seqlens=lens, seed=seed)
+    qd = np.random.default_rng(seed).standard_normal((len(lens), hq, d)).astype(np.float16)
+    s = np.exp(np.random.default_rng(seed).uniform(-1, 1, (hkv, d))).astype(np.float32)
+    _say("decode fused runs", len(lens), max(lens), d, hq, hkv)
+    _decode_and_compare(h, qd, k, v, cu, s, max(lens), seqs=seqs, kv_heads=kv_heads)
+
+
 def test_decode_cache_append(h):
     """The cache grows one token at a time: the K^ row of a new token
     quantized alone, and the V^ block holding it re-quantized from that
