@@ -608,8 +608,8 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (NT * RP <= 4 ? 4 : 2)) k_deco
 }
 
 // ---------------------------------------------------------------------------
-// 1+2. Scores and splits in one kernel, where the score runs and the splits
-// have the same length (kFusedRun blocks).  A wave computes its run's scores
+// 1+2. Scores and splits in one kernel, once the splits alone fill the chip
+// (runs of the split length).  A wave computes its run's scores
 // into LDS, publishes each row's maximum over the run (tagged with the call's
 // epoch), takes the running maximum entering the run as the maximum of the
 // earlier runs' maxima of its sequence, and runs the split from LDS: the
@@ -617,18 +617,17 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (NT * RP <= 4 ? 4 : 2)) k_deco
 // workgroups with lower indices, which each XCD dispatches first, so the
 // lowest unfinished workgroup is always running; a spin limit still ends
 // every wait.
-constexpr int kFusedRun = 8;
 constexpr int kLookBatch = 4;                    // run maxima per lane per round
 constexpr int kSpinLimit = 1 << 20;
 
-template <int G, int RP, int NORM, bool DEBUG>
+template <int G, int RP, int NORM, bool DEBUG, int RUN>
 __global__ void __launch_bounds__(64 * kMaxWaves, (G * RP <= 2 ? 4 : 2)) k_decode_fused(DecodeArgs a) {
-  __shared__ __align__(16) ScoreLds<G, kFusedRun> sl;
+  __shared__ __align__(16) ScoreLds<G, RUN> sl;
   __shared__ __align__(16) uint8_t lds_p[kMaxWaves][8 * 64];
   WaveSpan w;
-  if (!wave_span(a, kFusedRun, w)) return;
+  if (!wave_span(a, RUN, w)) return;
   const int wave = (int)(threadIdx.x >> 6), lane = threadIdx.x & 63, kq = lane & 15;
-  score_run<G, kFusedRun>(a, w, sl);
+  score_run<G, RUN>(a, w, sl);
   const int nb = w.J1 - w.J0;
   if (lane < w.grp) {
     half_t rm = sl.m[wave][lane][0];
@@ -669,21 +668,22 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (G * RP <= 2 ? 4 : 2)) k_decod
     for (int o = 1; o < 16; o <<= 1) mm = fmaxf(mm, __shfl_xor(mm, o));
     m_in[p] = (half_t)mm;
   }
-  split_run<2 * G, RP, NORM, DEBUG, kFusedRun, true>(a, w, lds_p[wave], &sl.s[wave][0][0], &sl.m[wave][0][0], m_in);
+  split_run<2 * G, RP, NORM, DEBUG, RUN, true>(a, w, lds_p[wave], &sl.s[wave][0][0], &sl.m[wave][0][0], m_in);
 }
 
 // ---------------------------------------------------------------------------
-// 3. Merge.  One workgroup per row (b, query head).  Each split wrote its l,
+// 3. Merge.  One workgroup per row (b, query head), or per (row, channel
+// slice) when there are few rows.  Each split wrote its l,
 // the product of its blocks' rescale factors r_J = E(fp16(m_{J-1} - m_J))
 // (in block order) and its running maximum after its last block.  Wave 0
 // turns the products into R_s = the product over all later splits (a backward
-// scan, 64 splits at a time); the partial sums, loaded before the scan, are
-// then weighted and added, thread (part, channel) taking every parts-th
-// split, and the parts combined through LDS.
+// scan, 64 splits at a time, which also sums l_s R_s); the partial sums,
+// loaded before the scan, are then weighted and added, thread (part,
+// channel) taking every parts-th split, and the parts combined through LDS.
 constexpr int kMergeThreads = 512;
 
 __global__ void __launch_bounds__(kMergeThreads) k_decode_merge(DecodeArgs a) {
-  extern __shared__ float R[];                    // [n_split], then partial sums
+  extern __shared__ float R[];                    // [n_split], then partial sums, then the l sum
   const int row = blockIdx.x;                     // b * hq + head
   const int b = row / a.hq, head = row % a.hq;
   const int L = dseq_len(a.cu, b, a.S);
@@ -692,11 +692,13 @@ __global__ void __launch_bounds__(kMergeThreads) k_decode_merge(DecodeArgs a) {
   const int ns = (nblk + a.bps - 1) / a.bps;
   const int tid = threadIdx.x, lane = tid & 63;
   const int D = a.D;
-  const int parts = kMergeThreads / D;            // 2, 4 or 8 threads per channel
-  float* acc_s = R + a.n_split;                   // [parts][D] and [parts] l sums
+  const int CW = D / (int)gridDim.y;              // this workgroup's channels
+  const int parts = kMergeThreads / CW;           // threads per channel
+  float* acc_s = R + a.n_split;                   // [parts][CW]
+  float* lsum_s = acc_s + parts * CW;
   const float4* sp = a.spart + (size_t)row * a.n_split;
   // the partial sums do not depend on the scan: load them first
-  const int ch = tid % D, part = tid / D;
+  const int c = tid % CW, part = tid / CW, ch = (int)blockIdx.y * CW + c;
   constexpr int kMaxHeld = 16;
   float po[kMaxHeld];
   const float* op = a.opart + (size_t)row * a.n_split * D + ch;
@@ -705,39 +707,44 @@ __global__ void __launch_bounds__(kMergeThreads) k_decode_merge(DecodeArgs a) {
     const int s = part + k * parts;
     po[k] = s < ns ? op[(size_t)s * D] : 0.0f;
   }
+  // wave 0: R_s backwards, 64 splits at a time, and l = sum_s l_s R_s
   if (tid < 64) {
-    float tail = 1.0f;
+    float tail = 1.0f, lpart = 0.0f;
     for (int s1 = ns; s1 > 0; s1 -= 64) {
       const int sidx = s1 - 1 - lane;
-      const float v = sidx >= 0 ? sp[sidx].y : 1.0f;
-      float incl = v;
+      const float4 v = sidx >= 0 ? sp[sidx] : make_float4(0.0f, 1.0f, 0.0f, 0.0f);
+      float incl = v.y;
 #pragma unroll
       for (int o = 1; o < 64; o <<= 1) {
         const float t = __shfl_up(incl, o);
         if (lane >= o) incl *= t;
       }
       const float excl = __shfl_up(incl, 1);
-      if (sidx >= 0) R[sidx] = tail * (lane == 0 ? 1.0f : excl);
+      const float rs = tail * (lane == 0 ? 1.0f : excl);
+      if (sidx >= 0) {
+        R[sidx] = rs;
+        lpart = __builtin_fmaf(v.x, rs, lpart);
+      }
       tail *= __shfl(incl, 63);
     }
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) lpart += __shfl_xor(lpart, o);
+    if (lane == 0) lsum_s[0] = lpart;
   }
   __syncthreads();
-  float acc = 0.0f, lacc = 0.0f;
+  float acc = 0.0f;
 #pragma unroll
   for (int k = 0; k < kMaxHeld; ++k) {
     const int s = part + k * parts;
     if (s < ns) acc = __builtin_fmaf(po[k], R[s], acc);
   }
   for (int s = part + kMaxHeld * parts; s < ns; s += parts) acc = __builtin_fmaf(op[(size_t)s * D], R[s], acc);
-  if (ch == 0)
-    for (int s = part; s < ns; s += parts) lacc = __builtin_fmaf(sp[s].x, R[s], lacc);
-  acc_s[part * D + ch] = acc;
-  if (ch == 0) acc_s[parts * D + part] = lacc;
+  acc_s[part * CW + c] = acc;
   __syncthreads();
   if (part == 0) {
-    float o = acc, lsum = 0.0f;
-    for (int p = 1; p < parts; ++p) o += acc_s[p * D + ch];
-    for (int p = 0; p < parts; ++p) lsum += acc_s[parts * D + p];
+    float o = acc;
+    for (int p = 1; p < parts; ++p) o += acc_s[p * CW + c];
+    const float lsum = lsum_s[0];
     a.o[(size_t)row * D + ch] = (half_t)(o * (1.0f / lsum));
     if (ch == 0) a.lse[(size_t)head * a.batch + b] = sp[ns - 1].z * 0.69314718055994531f + logf(lsum);
   }
@@ -764,7 +771,7 @@ int maxima_stride(int NB) { return (NB + 7) & ~7; }
 
 struct DecodePlan {
   int waves, head_groups, run, bps;
-  bool fused;              // one kernel for scores and splits (run == bps == kFusedRun)
+  bool fused;              // one kernel for scores and splits
 };
 
 DecodePlan plan_decode(int batch, int hkv, int NB) {
@@ -773,7 +780,9 @@ DecodePlan plan_decode(int batch, int hkv, int NB) {
   p.head_groups = (hkv + p.waves - 1) / p.waves;
   p.run = pick_run(p.head_groups, batch, NB);
   p.bps = pick_split(p.head_groups, batch, NB);
-  p.fused = p.run == kFusedRun && p.bps == kFusedRun;
+  // one kernel for scores and splits once the splits fill the chip; below
+  // that the score kernel's shorter runs give the score phase more workgroups
+  p.fused = (long)p.head_groups * batch * ((NB + p.bps - 1) / p.bps) >= kMinSplitWorkgroups;
   return p;
 }
 
@@ -834,14 +843,23 @@ void launch_split_run(const DecodeArgs& a, int grp, int norm, bool debug, dim3 g
   }
 }
 
+template <int G, int RP, int RUN>
+void launch_fused_run(const DecodeArgs& a, int norm, bool debug, dim3 grid, dim3 block, hipStream_t st) {
+  if (norm == 0) {
+    if (debug) k_decode_fused<G, RP, 0, true, RUN><<<grid, block, 0, st>>>(a);
+    else k_decode_fused<G, RP, 0, false, RUN><<<grid, block, 0, st>>>(a);
+  } else {
+    if (debug) k_decode_fused<G, RP, 1, true, RUN><<<grid, block, 0, st>>>(a);
+    else k_decode_fused<G, RP, 1, false, RUN><<<grid, block, 0, st>>>(a);
+  }
+}
+
 template <int G, int RP>
 void launch_fused_rows(const DecodeArgs& a, int norm, bool debug, dim3 grid, dim3 block, hipStream_t st) {
-  if (norm == 0) {
-    if (debug) k_decode_fused<G, RP, 0, true><<<grid, block, 0, st>>>(a);
-    else k_decode_fused<G, RP, 0, false><<<grid, block, 0, st>>>(a);
-  } else {
-    if (debug) k_decode_fused<G, RP, 1, true><<<grid, block, 0, st>>>(a);
-    else k_decode_fused<G, RP, 1, false><<<grid, block, 0, st>>>(a);
+  switch (a.bps) {
+    case 8: launch_fused_run<G, RP, 8>(a, norm, debug, grid, block, st); break;
+    case 4: launch_fused_run<G, RP, 4>(a, norm, debug, grid, block, st); break;
+    default: launch_fused_run<G, RP, 2>(a, norm, debug, grid, block, st); break;
   }
 }
 
@@ -931,10 +949,14 @@ hipError_t launch_decode(const DecodeLaunch& d, hipStream_t st) {
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (d.ev && (e = hipEventRecord(d.ev[1], st)) != hipSuccess) return e;
-  const int parts = kMergeThreads / d.D;
-  const size_t lds3 = ((size_t)a.n_split + (size_t)parts * d.D + parts) * sizeof(float);
+  // few rows: each row's channels are split over several workgroups (at
+  // least 32 channels each), so that every thread holds few partials
+  const long rows = (long)d.batch * d.hq;
+  int slices = 1;
+  while (rows * slices < kMinSplitWorkgroups && d.D / (2 * slices) >= 32) slices *= 2;
+  const size_t lds3 = ((size_t)a.n_split + kMergeThreads + 1) * sizeof(float);
   if ((e = allow_lds(k_decode_merge, lds3)) != hipSuccess) return e;
-  k_decode_merge<<<dim3(d.batch * d.hq), dim3(kMergeThreads), lds3, st>>>(a);
+  k_decode_merge<<<dim3((unsigned)rows, slices), dim3(kMergeThreads), lds3, st>>>(a);
   return hipGetLastError();
 }
 

@@ -112,6 +112,12 @@ def test_decode_workspace_sizes(lib):
     rows = 2 * 32
     want = rows * 64 * 64 * 2 + rows * 64 * 2 + rows * 32 * 128 * 4 + rows * 32 * 16
     assert lib.hifa4_decode_workspace_bytes(ctypes.byref(p)) == want
+    # 8 sequences of 4096 tokens: splits of 2 blocks fill 256 workgroups, so
+    # one kernel takes scores and splits (run maxima instead of scores)
+    p = _p(batch=8, max_seqlen=4096, num_heads_q=32, num_heads_kv=8)
+    rows = 8 * 32
+    want = rows * 32 * 128 * 4 + rows * 32 * 16 + rows * 32 * 8
+    assert lib.hifa4_decode_workspace_bytes(ctypes.byref(p)) == want
     # 100 tokens (2 blocks) pad the block maxima of a row to 8 entries
     p = _p(batch=3, max_seqlen=100, num_heads_q=4, num_heads_kv=1)
     rows = 3 * 4

@@ -149,12 +149,14 @@ def test_decode_many_splits(h, lens, d, hq, hkv, seed):
     ((3648, 3600, 3700, 3500, 3648, 3100, 3648, 3648), 64, 64, 64, 15, [0, 2, 5], [0, 37, 63]),
     # GQA x8 (two rows per softmax lane pass), 256 blocks in 2 workgroups of kv heads
     ((16384, 16000, 16384, 15000, 16384, 16300, 16384, 9000), 64, 128, 16, 16, [1, 7], [0, 9, 15]),
+    # 64 blocks: runs and splits of 2, GQA x4, D=128
+    ((4096, 4000, 4096, 3900, 4096, 4033, 4096, 2000), 128, 8, 2, 17, [0, 3, 7], [0, 1]),
 ])
 def test_decode_fused_runs(h, lens, d, hq, hkv, seed, seqs, kv_heads):
-    """Shapes where the score runs and the splits both take 8 blocks, so one
-    kernel computes the scores into LDS, publishes each row's run maximum and
-    reads the earlier runs' maxima of its sequence: every P^ code of the
-    sampled rows bit-exact."""
+    """Shapes whose splits fill the chip, so one kernel computes the scores
+    of a split's blocks into LDS, publishes each row's run maximum and reads
+    the earlier runs' maxima of its sequence: every P^ code of the sampled
+    rows bit-exact."""
     _, k, v, cu = small_case(heads_q=hkv, heads_kv=hkv, head_dim=d, seqlens=lens, seed=seed)
     qd = np.random.default_rng(seed).standard_normal((len(lens), hq, d)).astype(np.float16)
     s = np.exp(np.random.default_rng(seed).uniform(-1, 1, (hkv, d))).astype(np.float32)
