@@ -377,12 +377,48 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (G <= 2 ? 4 : 2)) k_decode_sco
 // from where lane (row l & 31, half h) reads its two operands.  B = 32
 // channels of the block's V^ groups; per 32-channel tile the two MFMAs give
 // the exact block sums, and O[row][ch] = fma(O, r_row, dot * b_V/16 * b_P/16).
+constexpr int kLookBatch = 4;                    // run maxima per lane per round
+constexpr int kSpinLimit = 1 << 20;
+
+// The running maximum entering run w.part of the lane's softmax row (pass
+// p): the maximum of the earlier runs' epoch-tagged maxima of the sequence,
+// 16 lanes per row, kLookBatch words each per round, every load of a round
+// in flight before the first is checked; a spin limit ends every wait.
+__device__ __forceinline__ float look_back(const DecodeArgs& a, const WaveSpan& w, int row) {
+  const int kq = threadIdx.x & 15;
+  const uint64_t* f = a.runmax + (w.row0 + row) * a.n_split;
+  float mm = -__builtin_inff();
+  for (int q0 = 0; q0 < w.part; q0 += 16 * kLookBatch) {
+    uint64_t wd[kLookBatch];
+#pragma unroll
+    for (int k = 0; k < kLookBatch; ++k) {
+      const int q = q0 + 16 * k + kq;
+      wd[k] = q < w.part ? __hip_atomic_load(f + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
+    }
+#pragma unroll
+    for (int k = 0; k < kLookBatch; ++k) {
+      const int q = q0 + 16 * k + kq;
+      if (q < w.part) {
+        uint64_t v = wd[k];
+        for (int it = 0; (uint32_t)(v >> 32) != a.epoch && it < kSpinLimit; ++it) {
+          __builtin_amdgcn_s_sleep(2);
+          v = __hip_atomic_load(f + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        mm = fmaxf(mm, (float)__builtin_bit_cast(half_t, (uint16_t)v));
+      }
+    }
+  }
+  return mm;
+}
+
 // FROM_LDS: the scores and block maxima of the split's blocks are in this
-// wave's LDS (lsc [8 rows][BPS * 64], lmx [8 rows][BPS]) and m_in holds the
-// running maximum entering the split per pass; otherwise both come from HBM.
+// wave's LDS (lsc [8 rows][BPS * 64], lmx [8 rows][BPS]) and the running
+// maximum entering the split comes from the earlier runs' published maxima
+// (look_back, once the first V^ blocks are in flight); otherwise all of it
+// comes from HBM.
 template <int NT, int RP, int NORM, bool DEBUG, int BPS, bool FROM_LDS>
 __device__ __forceinline__ void split_run(const DecodeArgs& a, const WaveSpan& w, uint8_t* lp, const half_t* lsc,
-                                          const half_t* lmx, const half_t* m_in) {
+                                          const half_t* lmx) {
   constexpr int kBlocksPerSplit = BPS;
   constexpr int D = 32 * NT;
   const int lane = threadIdx.x & 63, n = lane & 31, h = lane >> 5;
@@ -466,10 +502,10 @@ __device__ __forceinline__ void split_run(const DecodeArgs& a, const WaveSpan& w
   }
 #pragma unroll
   for (int p = 0; p < RP; ++p) {
-    float mm = fmaxf((float)pm[p][0], (float)pm[p][1]);
+    float mm = FROM_LDS ? look_back(a, w, prow[p]) : fmaxf((float)pm[p][0], (float)pm[p][1]);
 #pragma unroll
     for (int o = 1; o < 16; o <<= 1) mm = fmaxf(mm, __shfl_xor(mm, o));
-    m[p] = FROM_LDS ? m_in[p] : (half_t)mm;
+    m[p] = (half_t)mm;
   }
   float O[NT][4];
 #pragma unroll
@@ -604,7 +640,7 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (NT * RP <= 4 ? 4 : 2)) k_deco
   __shared__ __align__(16) uint8_t lds_p[kMaxWaves][8 * 64];
   WaveSpan w;
   if (!wave_span(a, BPS, w)) return;
-  split_run<NT, RP, NORM, DEBUG, BPS, false>(a, w, lds_p[threadIdx.x >> 6], nullptr, nullptr, nullptr);
+  split_run<NT, RP, NORM, DEBUG, BPS, false>(a, w, lds_p[threadIdx.x >> 6], nullptr, nullptr);
 }
 
 // ---------------------------------------------------------------------------
@@ -617,16 +653,13 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (NT * RP <= 4 ? 4 : 2)) k_deco
 // workgroups with lower indices, which each XCD dispatches first, so the
 // lowest unfinished workgroup is always running; a spin limit still ends
 // every wait.
-constexpr int kLookBatch = 4;                    // run maxima per lane per round
-constexpr int kSpinLimit = 1 << 20;
-
 template <int G, int RP, int NORM, bool DEBUG, int RUN>
 __global__ void __launch_bounds__(64 * kMaxWaves, (G * RP <= 2 ? 4 : 2)) k_decode_fused(DecodeArgs a) {
   __shared__ __align__(16) ScoreLds<G, RUN> sl;
   __shared__ __align__(16) uint8_t lds_p[kMaxWaves][8 * 64];
   WaveSpan w;
   if (!wave_span(a, RUN, w)) return;
-  const int wave = (int)(threadIdx.x >> 6), lane = threadIdx.x & 63, kq = lane & 15;
+  const int wave = (int)(threadIdx.x >> 6), lane = threadIdx.x & 63;
   score_run<G, RUN>(a, w, sl);
   const int nb = w.J1 - w.J0;
   if (lane < w.grp) {
@@ -636,39 +669,7 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (G * RP <= 2 ? 4 : 2)) k_decod
     __hip_atomic_store(a.runmax + (w.row0 + lane) * a.n_split + w.part, word, __ATOMIC_RELAXED,
                        __HIP_MEMORY_SCOPE_AGENT);
   }
-  // 16 lanes per softmax row, kLookBatch run maxima each per round, every
-  // load of a round issued before the first is checked
-  half_t m_in[RP];
-#pragma unroll
-  for (int p = 0; p < RP; ++p) {
-    const int r = 4 * p + (lane >> 4);
-    const uint64_t* f = a.runmax + (w.row0 + (r < w.grp ? r : 0)) * a.n_split;
-    float mm = -__builtin_inff();
-    for (int q0 = 0; q0 < w.part; q0 += 16 * kLookBatch) {
-      uint64_t wd[kLookBatch];
-#pragma unroll
-      for (int k = 0; k < kLookBatch; ++k) {
-        const int q = q0 + 16 * k + kq;
-        wd[k] = q < w.part ? __hip_atomic_load(f + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
-      }
-#pragma unroll
-      for (int k = 0; k < kLookBatch; ++k) {
-        const int q = q0 + 16 * k + kq;
-        if (q < w.part) {
-          uint64_t v = wd[k];
-          for (int it = 0; (uint32_t)(v >> 32) != a.epoch && it < kSpinLimit; ++it) {
-            __builtin_amdgcn_s_sleep(2);
-            v = __hip_atomic_load(f + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          }
-          mm = fmaxf(mm, (float)__builtin_bit_cast(half_t, (uint16_t)v));
-        }
-      }
-    }
-#pragma unroll
-    for (int o = 1; o < 16; o <<= 1) mm = fmaxf(mm, __shfl_xor(mm, o));
-    m_in[p] = (half_t)mm;
-  }
-  split_run<2 * G, RP, NORM, DEBUG, RUN, true>(a, w, lds_p[wave], &sl.s[wave][0][0], &sl.m[wave][0][0], m_in);
+  split_run<2 * G, RP, NORM, DEBUG, RUN, true>(a, w, lds_p[wave], &sl.s[wave][0][0], &sl.m[wave][0][0]);
 }
 
 // ---------------------------------------------------------------------------
