@@ -10,7 +10,8 @@
 // decode row has too little work per sequence for one workgroup, so the key
 // range is split; the split must not change any P^ code, because P^ depends
 // on the running maximum entering each 64-key block.  Three kernels keep every
-// decision of the sequential loop:
+// decision of the sequential loop (where the splits alone fill the chip, the
+// first two are one kernel: see "1+2" below):
 //   1. scores: per (sequence, run of 64-key blocks, kv head) the query rows
 //      of the GQA group are smoothed and quantized (Q^ = HIF4(fp16(q s))),
 //      then the fp16 scores S2 are stored with each row's block maximum;
