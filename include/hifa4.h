@@ -141,6 +141,7 @@ typedef struct {
   void* debug_p_meta;
   void** timing_events;
   int32_t q_mean;
+  int32_t test_decode_no_publish;  /* testing only, hifa4_decode_fwd: see there */
 } hifa4_fwd_options;
 
 /* Host-side calibration report (Table 1 statistics and the gate decision). */
@@ -276,7 +277,18 @@ size_t hifa4_decode_workspace_bytes(const hifa4_problem* p);
  *    HIFA4_OPERANDS_HIF4 and q_mean 0 (the cache carries no key sums), else
  *    HIFA4_ERR_UNSUPPORTED; num_heads_q / num_heads_kv must be <= 8 (else
  *    HIFA4_ERR_UNSUPPORTED).
- * workspace: DEVICE, >= hifa4_decode_workspace_bytes(p).  Asynchronous. */
+ * workspace: DEVICE, >= hifa4_decode_workspace_bytes(p).  Asynchronous.
+ * Where the splits of the key range fill the GPU (at least 256 workgroups),
+ * scores and splits run in one kernel in which each split waits, with a
+ * bounded spin, for the run maxima that the splits before it in the same row
+ * publish (tagged with a per-call value; the last kernel of the call clears
+ * them, so no word of an earlier call, eager or replayed from a graph,
+ * satisfies a wait).  The waits end because every GPU engine dispatches the
+ * workgroups of a grid in index order and each waits only on lower indices;
+ * if a wait nevertheless gives up, that row's o and lse are NaN (never a
+ * silently wrong value).  opt->test_decode_no_publish != 0 (testing only)
+ * publishes nothing and lets every wait give up after 16 polls, so that the
+ * rows of every split after the first come out NaN. */
 hifa4_status hifa4_decode_fwd(const hifa4_problem* p, const hifa4_fwd_options* opt,
                               const void* q, const void* k_codes, const void* k_meta,
                               const void* v_codes, const void* v_meta, const float* s,

@@ -42,7 +42,8 @@ class Problem(ctypes.Structure):
 class FwdOptions(ctypes.Structure):
     _fields_ = [("norm", ctypes.c_int32), ("operands", ctypes.c_int32), ("smooth_qk", ctypes.c_int32),
                 ("debug_p_codes", ctypes.c_void_p), ("debug_p_meta", ctypes.c_void_p),
-                ("timing_events", ctypes.c_void_p), ("q_mean", ctypes.c_int32)]
+                ("timing_events", ctypes.c_void_p), ("q_mean", ctypes.c_int32),
+                ("test_decode_no_publish", ctypes.c_int32)]
 
 
 class CalibReport(ctypes.Structure):
@@ -336,7 +337,8 @@ def hifa4_decode_workspace_bytes(shape: Shape) -> int:
 
 def hifa4_decode_fwd(q, k_codes, k_meta, v_codes, v_meta, s=None, cu_seqlens=None, max_seqlen=None,
                      norm: int = NORM_PREORDER, smooth_qk: Optional[bool] = None, debug_p: bool = False,
-                     out=None, lse=None, workspace: Optional[Workspace] = None, timing_events=None):
+                     out=None, lse=None, workspace: Optional[Workspace] = None, timing_events=None,
+                     test_no_publish: bool = False):
     """One decode step over a packed HIF4 cache: q [B, Hq, D] fp16 is the query
     of each sequence's newest token; the cache is the output of
     hifa4_quantize_qk (K^, same s) and hifa4_quantize_v (V^) over the cached
@@ -371,7 +373,8 @@ def hifa4_decode_fwd(q, k_codes, k_meta, v_codes, v_meta, s=None, cu_seqlens=Non
     if timing_events is not None:
         ev_arr = (ctypes.c_void_p * 3)(*[e.cuda_event for e in timing_events])
     opt = FwdOptions(norm, OPERANDS_HIF4, 1 if smooth_qk else 0, _ptr(pc), _ptr(pm),
-                     ctypes.cast(ev_arr, ctypes.c_void_p) if ev_arr is not None else None, 0)
+                     ctypes.cast(ev_arr, ctypes.c_void_p) if ev_arr is not None else None, 0,
+                     1 if test_no_publish else 0)
     p = sh.problem()
     need = int(lib.hifa4_decode_workspace_bytes(ctypes.byref(p)))
     ws = (workspace or _default_ws).get(need, dev)

@@ -252,6 +252,7 @@ hifa4_status hifa4_decode_fwd(const hifa4_problem* p, const hifa4_fwd_options* o
   dl.hkv = p->num_heads_kv;
   dl.D = p->head_dim;
   dl.norm = opt->norm;
+  dl.test_no_publish = opt->test_decode_no_publish ? 1 : 0;
   dl.c = (float)(1.4426950408889634 / std::sqrt((double)p->head_dim));
   e = hifa4::launch_decode(dl, hs);
   if (e != hipSuccess) return hip_fail(e, "decode kernels");

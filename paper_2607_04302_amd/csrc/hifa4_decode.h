@@ -21,6 +21,7 @@ struct DecodeLaunch {
   uint8_t* ws;
   hipEvent_t* ev;          // optional; ev[1] is recorded before the merge kernel
   int batch, S, NB, hq, hkv, D, norm;
+  int test_no_publish;     // testing: no run maxima published, waits give up after 16 polls
   float c;
 };
 

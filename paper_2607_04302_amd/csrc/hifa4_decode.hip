@@ -153,8 +153,11 @@ struct DecodeArgs {
   int batch, S, NB, hq, hkv, D, n_split, waves, bps;
   int mxs;                 // row stride of the block maxima: NB rounded up to 8
   float c;
-  uint64_t* runmax;        // fused path: [batch, Hq, n_split] run maxima, epoch-tagged
+  uint64_t* runmax;        // fused path: [batch, Hq, n_split] run maxima, epoch-tagged;
+                           // the merge kernel clears each row's words after the splits
   uint32_t epoch;          // fused path: this call's tag (never 0)
+  int spin_limit;          // polls before a look-back wait gives up
+  int publish;             // 0: the fused kernel publishes no run maxima (testing the give-up)
 };
 
 // One wave's share of a workgroup: kv head hk of sequence b, blocks
@@ -384,11 +387,14 @@ constexpr int kSpinLimit = 1 << 20;
 // The running maximum entering run w.part of the lane's softmax row (pass
 // p): the maximum of the earlier runs' epoch-tagged maxima of the sequence,
 // 16 lanes per row, kLookBatch words each per round, every load of a round
-// in flight before the first is checked; a spin limit ends every wait.
-__device__ __forceinline__ float look_back(const DecodeArgs& a, const WaveSpan& w, int row) {
+// in flight before the first is checked.  A spin limit ends every wait; a
+// wait that gives up sets `lost` (the split then poisons its partial, so the
+// row's O and LSE come out NaN instead of silently wrong).
+__device__ __forceinline__ float look_back(const DecodeArgs& a, const WaveSpan& w, int row, bool& lost) {
   const int kq = threadIdx.x & 15;
   const uint64_t* f = a.runmax + (w.row0 + row) * a.n_split;
   float mm = -__builtin_inff();
+  lost = false;
   for (int q0 = 0; q0 < w.part; q0 += 16 * kLookBatch) {
     uint64_t wd[kLookBatch];
 #pragma unroll
@@ -401,11 +407,12 @@ __device__ __forceinline__ float look_back(const DecodeArgs& a, const WaveSpan& 
       const int q = q0 + 16 * k + kq;
       if (q < w.part) {
         uint64_t v = wd[k];
-        for (int it = 0; (uint32_t)(v >> 32) != a.epoch && it < kSpinLimit; ++it) {
+        for (int it = 0; (uint32_t)(v >> 32) != a.epoch && it < a.spin_limit; ++it) {
           __builtin_amdgcn_s_sleep(2);
           v = __hip_atomic_load(f + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
-        mm = fmaxf(mm, (float)__builtin_bit_cast(half_t, (uint16_t)v));
+        if ((uint32_t)(v >> 32) == a.epoch) mm = fmaxf(mm, (float)__builtin_bit_cast(half_t, (uint16_t)v));
+        else lost = true;
       }
     }
   }
@@ -501,12 +508,19 @@ __device__ __forceinline__ void split_run(const DecodeArgs& a, const WaveSpan& w
         }
       }
   }
+  bool lost[RP];                                 // a look-back wait of the row gave up
 #pragma unroll
   for (int p = 0; p < RP; ++p) {
-    float mm = FROM_LDS ? look_back(a, w, prow[p]) : fmaxf((float)pm[p][0], (float)pm[p][1]);
+    bool lp_ = false;
+    float mm = FROM_LDS ? look_back(a, w, prow[p], lp_) : fmaxf((float)pm[p][0], (float)pm[p][1]);
+    int lf = lp_ ? 1 : 0;
 #pragma unroll
-    for (int o = 1; o < 16; o <<= 1) mm = fmaxf(mm, __shfl_xor(mm, o));
+    for (int o = 1; o < 16; o <<= 1) {
+      mm = fmaxf(mm, __shfl_xor(mm, o));
+      lf |= __shfl_xor(lf, o);
+    }
     m[p] = (half_t)mm;
+    lost[p] = lf != 0;
   }
   float O[NT][4];
 #pragma unroll
@@ -632,7 +646,9 @@ __device__ __forceinline__ void split_run(const DecodeArgs& a, const WaveSpan& w
 #pragma unroll
   for (int p = 0; p < RP; ++p) {
     const int r = 4 * p + (lane >> 4);
-    if (r < grp && kq == 0) a.spart[(row0 + r) * a.n_split + sp] = make_float4(l[p], prod[p], (float)m[p], 0.0f);
+    if (r < grp && kq == 0)
+      a.spart[(row0 + r) * a.n_split + sp] =
+          make_float4(lost[p] ? __builtin_nanf("") : l[p], prod[p], (float)m[p], 0.0f);
   }
 }
 
@@ -663,7 +679,7 @@ __global__ void __launch_bounds__(64 * kMaxWaves, (G * RP <= 2 ? 4 : 2)) k_decod
   const int wave = (int)(threadIdx.x >> 6), lane = threadIdx.x & 63;
   score_run<G, RUN>(a, w, sl);
   const int nb = w.J1 - w.J0;
-  if (lane < w.grp) {
+  if (lane < w.grp && a.publish) {
     half_t rm = sl.m[wave][lane][0];
     for (int i = 1; i < nb; ++i) rm = hmax(rm, sl.m[wave][lane][i]);
     const uint64_t word = ((uint64_t)a.epoch << 32) | (uint64_t)__builtin_bit_cast(uint16_t, rm);
@@ -693,6 +709,11 @@ __global__ void __launch_bounds__(kMergeThreads) k_decode_merge(DecodeArgs a) {
   if (nblk == 0) return;
   const int ns = (nblk + a.bps - 1) / a.bps;
   const int tid = threadIdx.x, lane = tid & 63;
+  // fused path: the splits have read this row's run maxima; clearing them here
+  // (a kernel write, so it is part of a captured graph too) means that no word
+  // of a finished call can satisfy a later call's wait, whatever its epoch
+  if (a.runmax != nullptr && blockIdx.y == 0)
+    for (int s = tid; s < ns; s += kMergeThreads) a.runmax[(size_t)row * a.n_split + s] = 0;
   const int D = a.D;
   const int CW = D / (int)gridDim.y;              // this workgroup's channels
   const int parts = kMergeThreads / CW;           // threads per channel
@@ -801,8 +822,10 @@ void decode_offsets(int batch, int hq, int D, int NB, const DecodePlan& pl, size
 }
 
 // Epoch tags of the fused path: a fresh value per call, starting from a
-// random point so that words another process left in reused memory do not
-// match.
+// random point.  Tags only separate eager calls; under graph replay the tag
+// is the captured one, and what keeps a replay from reading the previous
+// replay's words is the merge kernel clearing them (a cleared word never
+// matches, the tag is never 0).
 uint32_t next_epoch() {
   static std::atomic<uint32_t> counter{(uint32_t)std::random_device{}()};
   uint32_t e = counter.fetch_add(1) + 1;
@@ -910,6 +933,8 @@ hipError_t launch_decode(const DecodeLaunch& d, hipStream_t st) {
   a.spart = reinterpret_cast<float4*>(ws + off[3]);
   a.runmax = pl.fused ? reinterpret_cast<uint64_t*>(ws + off[4]) : nullptr;
   a.epoch = pl.fused ? next_epoch() : 0;
+  a.spin_limit = d.test_no_publish ? 16 : kSpinLimit;
+  a.publish = d.test_no_publish ? 0 : 1;
   a.o = d.o;
   a.lse = d.lse;
   a.dbg_codes = d.dbg_codes;

@@ -265,3 +265,81 @@ def test_decode_graph_replay(h):
         h.hifa4_decode_fwd(qd, kc, km, vc, vm, s_t, cu_seqlens=cu_t, max_seqlen=700)   # eager work between
         torch.cuda.synchronize()
     _say("decode graph replays ok")
+
+
+def _fused_case():
+    """8 sequences of about 4096 tokens, 2 kv heads, GQA x4, D=128: 64 blocks
+    per row in splits of 2, 256 split workgroups, so scores and splits run in
+    one kernel that waits on run maxima."""
+    lens = (4096, 4000, 4096, 3900, 4096, 4033, 4096, 2000)
+    _, k, v, cu = small_case(heads_q=2, heads_kv=2, head_dim=128, seqlens=lens, seed=31)
+    s = np.exp(np.random.default_rng(31).uniform(-1, 1, (2, 128))).astype(np.float32)
+    return lens, k, v, cu, s
+
+
+def test_decode_graph_replay_fused(h):
+    """The fused decode step captured once and replayed back to back with a
+    new query written in place before each replay (no eager decode call in
+    between): every replay equals an eager call on the same query bit for
+    bit, and its P^ codes equal the oracle's on sampled rows.  A replay reuses
+    the captured call's tag, so this fails if a split can take the previous
+    replay's run maxima for its own."""
+    import torch
+    lens, k, v, cu, s = _fused_case()
+    hq, hkv, d = 8, 2, 128
+    kc, km, vc, vm, cu_t = _build_cache(h, k, v, s, cu, max(lens))
+    s_t = to_gpu(s)
+    rng = np.random.default_rng(32)
+    queries = [(rng.standard_normal((len(lens), hq, d)) * (1.0 + 2.0 * i)).astype(np.float16) for i in range(3)]
+    q_buf = to_gpu(queries[0])
+    ws = h.Workspace()
+    kw = dict(cu_seqlens=cu_t, max_seqlen=max(lens), workspace=ws, debug_p=True)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        h.hifa4_decode_fwd(q_buf, kc, km, vc, vm, s_t, **kw)
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        g_o, g_l, g_pc, g_pm = h.hifa4_decode_fwd(q_buf, kc, km, vc, vm, s_t, **kw)
+    got = []
+    for qi in queries:
+        q_buf.copy_(to_gpu(qi))
+        graph.replay()
+        got.append((g_o.clone(), g_l.clone(), g_pc.clone(), g_pm.clone()))
+    torch.cuda.synchronize()
+    for i, qi in enumerate(queries):
+        _say("fused replay", i)
+        o, l, pc, pm = h.hifa4_decode_fwd(to_gpu(qi), kc, km, vc, vm, s_t, cu_seqlens=cu_t,
+                                          max_seqlen=max(lens), debug_p=True)
+        torch.cuda.synchronize()
+        assert torch.equal(got[i][0], o) and torch.equal(got[i][1], l), f"replay {i} differs from eager"
+        assert torch.equal(got[i][2], pc) and torch.equal(got[i][3], pm), f"replay {i} P^ differs from eager"
+        pc_n, pm_n = to_np(got[i][2]), to_np(got[i][3]).view(np.uint32)
+        for b in (0, 5):
+            k_seq, v_seq = k[cu[b]:cu[b + 1]], v[cu[b]:cu[b + 1]]
+            nb = -(-k_seq.shape[0] // 64)
+            for hk in range(hkv):
+                for j, r in enumerate(_oracle_row(qi[b], k_seq, v_seq, s, hk, hq // hkv, "preorder")):
+                    hh = hk * (hq // hkv) + j
+                    assert np.array_equal(pc_n[hh, b, :nb], r["p_codes"][0, :nb]), (i, b, hh)
+                    assert np.array_equal(pm_n[hh, b, :nb], r["p_meta"][0, :nb]), (i, b, hh)
+    _say("fused graph replays ok")
+
+
+def test_decode_wait_gives_up(h):
+    """The bounded wait of the fused kernel made to give up from the host (no
+    run maxima published, 16 polls per wait): every kernel ends and each row,
+    whose later splits all lost their wait, comes out NaN rather than
+    silently wrong; the next normal call is correct again."""
+    import torch
+    lens, k, v, cu, s = _fused_case()
+    hq, d = 8, 128
+    kc, km, vc, vm, cu_t = _build_cache(h, k, v, s, cu, max(lens))
+    qd = np.random.default_rng(33).standard_normal((len(lens), hq, d)).astype(np.float16)
+    o, l = h.hifa4_decode_fwd(to_gpu(qd), kc, km, vc, vm, to_gpu(s), cu_seqlens=cu_t, max_seqlen=max(lens),
+                              test_no_publish=True)
+    torch.cuda.synchronize()
+    assert torch.isnan(o).all() and torch.isnan(l).all(), "a wait that gave up must poison its row"
+    _say("decode give-up rows are NaN")
+    _decode_and_compare(h, qd, k, v, cu, s, max(lens), seqs=[1, 7], kv_heads=[0, 1])
