@@ -13,15 +13,18 @@ Readings fixed here (the paper is silent on them):
     V along tokens (64 tokens of one channel; a partial last group is zero
     padded), P along the 64 keys of a block -- every group lies along the
     contraction axis of its GEMM;
-  * scores: the softmax scale c = fp32(log2(e)/sqrt(D)) is folded into each
-    query group's scale, w_g = fp32(b_Q,g/4 * c) (b_Q,g the group's E6M2
-    base); per 64-channel group g the dot d_g of the Q operand values
-    (+-u*2^-sh, the dequantized values divided by b_Q,g/4) with the
-    dequantized K^ is exact; the fp32 accumulator takes fp32(d_0 * w_0), then
-    one fused multiply-add d_g * w_g + acc per further group (each rounded
-    once to fp32, nearest even), and S2 = fp16(acc) (nearest even).  The
-    softmax runs in base 2 (2^(S2-m) equals exp(S/sqrt(D) - m') exactly in
-    real arithmetic);
+  * scores (Algorithm 1's S = Q^K^T/sqrt(d), computed on the HIF4 matrix
+    unit): per 64-channel group g the term t_g = (dequantized Q^ group) .
+    (dequantized K^ group) is exact (a block-scaled product forms each
+    group's dot and applies both block scales without rounding; t_g has at
+    most 22 significant bits); the groups are summed in fp32 in contraction
+    order, S_acc = fp32(fp32(t_0 + t_1) + t_2) ..., each addition rounded
+    once (nearest even); then the score scale c = fp32(log2(e)/sqrt(D)) is
+    one fp32 multiply, and the product is converted to the fp16 the softmax
+    works in: S2 = fp16(fp32(S_acc * c)).  With Q-Mean the correction
+    mu_i * kappa_j (Algorithm 1's added term, after the group terms) is added
+    to S_acc with one rounding before the scale.  The softmax runs in base 2
+    (2^(S2-m) equals exp(S/sqrt(D) - m') exactly in real arithmetic);
   * running max m and the weights are fp16: m_new = max(m, rowmax S2),
     x = fp16(S2 - m_new), P16 = E(x), r = E(fp16(m - m_new));
   * P-Reordering: P^ = HIF4(P16 over the block), O <- r*O + P^ V^,
@@ -43,8 +46,8 @@ import numpy as np
 
 from . import hif4
 from .smooth import apply as smooth_apply
-from .fparith import fma_f32
-from .qmean import correction, key_sums, token_mean, zero_mean
+from . import qmean as _qmean
+from .qmean import key_sums, token_mean, zero_mean
 from .softmax16 import exp2_fp16, sub_fp16
 
 BLOCK = 64
@@ -91,26 +94,23 @@ def scores_hif4(q_op, q_base, khat, head_dim, corr=None):
     the Q group bases q_base [n, D/64] (E6M2 values) and the dequantized K^
     [L, D] (float64).
 
-    w_g = fp32(q_base/4 * c): the exact product rounded once.  Each group dot
-    d_g is exact in float64 and representable in fp32 (integer grid, at most
-    22 significant bits).  acc = fp32(d_0 * w_0) (the exact product rounded
-    once), then acc = fma32(d_g, w_g, acc) for g = 1, 2, ...; S2 = fp16(acc).
-    With Q-Mean, corr [n, L] (fp32, already scaled by c) is the accumulator's
-    starting value and the first group is fused onto it as well."""
+    t_g = (q_op_g * q_base_g/4) . khat_g, the exact dot of the dequantized
+    groups (float64 holds it exactly; it is also exact in fp32).  S_acc is
+    their fp32 sum in group order, each addition rounded once; with Q-Mean,
+    corr = (mu [n] fp16, kappa [L] fp32) and S_acc = fp32(S_acc + mu*kappa)
+    (the exact product added with one rounding).  S2 = fp16(fp32(S_acc*c))."""
     c = score_scale(head_dim)
-    w = (np.asarray(q_base, np.float64) / 4.0 * np.float64(c)).astype(np.float32)
-    acc = None if corr is None else np.asarray(corr, np.float32)
+    acc = None
     for g in range(head_dim // 64):
         sl = slice(64 * g, 64 * g + 64)
-        d = q_op[:, sl] @ khat[:, sl].T                       # exact
-        d32 = d.astype(np.float32)
-        assert np.array_equal(d32.astype(np.float64), d), "group dot not exact in fp32"
-        wg = w[:, g:g + 1]
-        if acc is None:
-            acc = (d * wg.astype(np.float64)).astype(np.float32)  # exact product, one rounding
-        else:
-            acc = fma_f32(d32, wg, acc)
-    return acc.astype(np.float16)
+        qdq = q_op[:, sl] * (np.asarray(q_base, np.float64)[:, g:g + 1] / 4.0)    # dequantized Q^ group
+        t = qdq @ khat[:, sl].T                                                    # exact
+        t32 = t.astype(np.float32)
+        assert np.array_equal(t32.astype(np.float64), t), "group term not exact in fp32"
+        acc = t32 if acc is None else (acc + t32)                                  # fp32 RNE
+    if corr is not None:
+        acc = _qmean.add_correction(acc, *corr)
+    return (acc * c).astype(np.float16)
 
 
 def scores_fp16(q, k, head_dim):
@@ -221,7 +221,7 @@ def attention_fwd(q, k, v, s=None, cu_seqlens=None, norm="preorder", operands="h
                 if q_mean:
                     mu = token_mean(qs[rr])
                     qf = quantize_rows(zero_mean(qs[rr], mu))
-                    corr = correction(mu, key_sums(ks), score_scale(d))
+                    corr = (mu, key_sums(ks))
                 else:
                     qf = quantize_rows(qs[rr])
                 khat = quantize_rows(ks)["xhat"].reshape(length, d)

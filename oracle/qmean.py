@@ -17,17 +17,19 @@ Readings fixed here (the paper names the operation but not its rounding):
     rounded once to fp16 (mu is an FP16 quantity of the GEMV);
   * Q_z = fp16(q~ - mu): the exact difference rounded once;
   * kappa_j = fp32(sum_c k~_jc): the exact sum rounded once to fp32;
-  * the correction is scaled like the rest of the score and enters the fp32
-    score accumulator first: cmu_i = fp32(mu_i * c) (c = fp32(log2(e)/sqrt(D))
-    the softmax scale), corr = fp32(cmu_i * kappa_j); each query group's term
-    d_g * w_g (w_g = fp32(b_Q,g/4 * c)) is then added by a fused multiply-add,
-    and S2 = fp16(acc) as without Q-Mean.  Algorithm 1 writes the correction
-    after the division by sqrt(d); scaling it by c with the rest of S is what
-    the identity above requires.
+  * the correction mu_i * kappa_j is added to the fp32 score accumulator
+    after the group terms (Algorithm 1 adds it after the product), the exact
+    product with one rounding, and is then scaled by c with the rest of the
+    score: S2 = fp16(fp32(fp32(S_acc + mu_i*kappa_j) * c)).  Scaling it with
+    the rest of S is what the identity above requires (Algorithm 1 writes the
+    correction after the division by sqrt(d), which only holds once the
+    correction carries the same scale).
 """
 from __future__ import annotations
 
 import numpy as np
+
+from .fparith import fma_f32
 
 
 def token_mean(q_tilde):
@@ -48,9 +50,8 @@ def key_sums(k_tilde):
     return np.asarray(k_tilde, np.float16).astype(np.float64).sum(axis=-1).astype(np.float32)
 
 
-def correction(mu, kappa, c):
-    """corr[i, j] = fp32(fp32(mu_i * c) * kappa_j).  Both products are exact
-    in float64 (fp16 times fp32, fp32 times fp32), so each is rounded once."""
-    cmu = (np.asarray(mu, np.float16).astype(np.float64) * np.float64(np.float32(c))).astype(np.float32)
-    return (cmu.astype(np.float64)[:, None]
-            * np.asarray(kappa, np.float32).astype(np.float64)[None, :]).astype(np.float32)
+def add_correction(acc, mu, kappa):
+    """fp32(acc[i, j] + mu_i * kappa_j): the exact product (fp16 times fp32)
+    added to the fp32 score accumulator with one rounding."""
+    return fma_f32(np.asarray(mu, np.float16).astype(np.float32)[:, None],
+                   np.asarray(kappa, np.float32)[None, :], acc)

@@ -221,11 +221,12 @@ def _one_term(d, head_dim):
 
 
 def test_score_rounds_to_fp32_then_fp16():
-    """S2 = fp16(acc), acc an fp32 value.  Witness (D = 64, base 4 so that
-    w = c): d = 1.386971354484558 (an fp32 value); the exact product d*c lies
-    above the fp16 midpoint M = 0.2501220703125 of 0.25 and 0.250244140625 but
-    rounds to M in fp32; M then rounds to the even 0.25, while a single
-    rounding of the exact product would give 0.250244140625."""
+    """S2 = fp16(fp32(S_acc * c)): the scaled score is an fp32 value before the
+    conversion to fp16.  Witness (D = 64, one group term d with base 4, so
+    S_acc = d): d = 1.386971354484558 (an fp32 value); the exact product d*c
+    lies above the fp16 midpoint M = 0.2501220703125 of 0.25 and
+    0.250244140625 but rounds to M in fp32; M then rounds to the even 0.25,
+    while a single rounding of the exact product would give 0.250244140625."""
     from fractions import Fraction
     d = float(np.float32(1.386971354484558))
     c = attention.score_scale(64)
@@ -236,48 +237,68 @@ def test_score_rounds_to_fp32_then_fp16():
     assert s2.dtype == np.float16 and float(s2[0, 0]) == 0.25
 
 
-def test_score_scale_is_folded_into_the_query_scale():
-    """w = fp32(b/4 * c) is rounded before it multiplies the group dot.
-    Witness (D = 64): b = 1.25, d = 48.6416015625.  fp16(fp32(d * w)) =
-    2.7421875, whereas scaling the exact group term d*b/4 by c afterwards
-    (fp16(fp32(fp32(d*b/4) * c))) gives 2.740234375."""
+def test_score_scale_multiplies_the_group_sum():
+    """The softmax scale multiplies the accumulated score once; it is not
+    folded into the query's block scale first.  Witness (D = 64): b = 1.25,
+    d = 48.6416015625: the group term d*b/4 is exact, fp16(fp32(fp32(d*b/4) * c))
+    = 2.740234375, whereas folding the scale (fp16(fp32(d * fp32(b/4 * c))))
+    gives 2.7421875."""
     from fractions import Fraction
     d, b = 48.6416015625, 1.25
     c = Fraction(float(attention.score_scale(64)))
-    w = _rn32(Fraction(b) / 4 * c)
-    assert _rn16(_rn32(Fraction(d) * w)) == Fraction(2.7421875)
     assert _rn16(_rn32(_rn32(Fraction(d) * Fraction(b) / 4) * c)) == Fraction(2.740234375)
+    assert _rn16(_rn32(Fraction(d) * _rn32(Fraction(b) / 4 * c))) == Fraction(2.7421875)
     q_op, khat = _one_term([d], 64)
     s2 = attention.scores_hif4(q_op, np.array([[b]]), khat, 64)
-    assert float(s2[0, 0]) == 2.7421875
+    assert float(s2[0, 0]) == 2.740234375
 
 
-def test_score_groups_accumulate_by_fused_multiply_add():
-    """acc = fp32(d_0 w_0), then acc = fp32(d_1 w_1 + acc) rounded once.
-    Witness (D = 128): d = (-61.828125, 26.4765625), b = (0.375, 0.875): the
-    fused form gives S2 = -0.0005917549133300781, a separate product and sum
-    -0.000591278076171875.  Swapping the groups' scales also changes S2."""
+def test_group_terms_sum_in_fp32():
+    """The group terms are added in fp32 (each addition rounded once) before
+    the scale.  Witness (D = 128): t = (-19.95166015625, -0.5801534652709961),
+    exact in fp32; fp16(fp32(fp32(t0 + t1) * c)) = -2.619140625, while the
+    exact sum scaled and rounded the same way gives -2.6171875."""
     from fractions import Fraction
-    d0, d1, b0, b1 = -61.828125, 26.4765625, 0.375, 0.875
+    t0, t1 = -19.95166015625, -0.5801534652709961
     c = Fraction(float(attention.score_scale(128)))
-    w0, w1 = _rn32(Fraction(b0) / 4 * c), _rn32(Fraction(b1) / 4 * c)
-    a0 = _rn32(Fraction(d0) * w0)
-    fused = _rn16(_rn32(Fraction(d1) * w1 + a0))
-    split = _rn16(_rn32(_rn32(Fraction(d1) * w1) + a0))
-    assert fused == Fraction(-0.0005917549133300781) and split == Fraction(-0.000591278076171875)
-    q_op, khat = _one_term([d0, d1], 128)
-    s2 = attention.scores_hif4(q_op, np.array([[b0, b1]]), khat, 128)
-    assert Fraction(float(s2[0, 0])) == fused
-    s2x = attention.scores_hif4(q_op, np.array([[b1, b0]]), khat, 128)
-    assert Fraction(float(s2x[0, 0])) != fused
+    assert _rn16(_rn32(_rn32(Fraction(t0) + Fraction(t1)) * c)) == Fraction(-2.619140625)
+    assert _rn16(_rn32((Fraction(t0) + Fraction(t1)) * c)) == Fraction(-2.6171875)
+    q_op, khat = _one_term([t0, t1], 128)
+    s2 = attention.scores_hif4(q_op, np.array([[4.0, 4.0]]), khat, 128)
+    assert float(s2[0, 0]) == -2.619140625
+
+
+def test_group_terms_sum_left_to_right():
+    """At D = 256 the four group terms are summed in contraction order,
+    ((t0 + t1) + t2) + t3.  Witness: t = (18.738555908203125,
+    -2.418212890625, -0.21242237091064453, -0.6583194732666016) gives
+    S2 = 1.3935546875; a pairwise sum (t0 + t1) + (t2 + t3) and the reversed
+    order both give 1.392578125, and so does the witness with its groups
+    reversed."""
+    from fractions import Fraction
+    t = [18.738555908203125, -2.418212890625, -0.21242237091064453, -0.6583194732666016]
+    c = Fraction(float(attention.score_scale(256)))
+    f = [Fraction(x) for x in t]
+    left = _rn32(_rn32(_rn32(f[0] + f[1]) + f[2]) + f[3])
+    pair = _rn32(_rn32(f[0] + f[1]) + _rn32(f[2] + f[3]))
+    assert _rn16(_rn32(left * c)) == Fraction(1.3935546875) and _rn16(_rn32(pair * c)) == Fraction(1.392578125)
+    q_op, khat = _one_term(t, 256)
+    ones = np.full((1, 4), 4.0)
+    assert float(attention.scores_hif4(q_op, ones, khat, 256)[0, 0]) == 1.3935546875
+    q_op, khat = _one_term(t[::-1], 256)
+    assert float(attention.scores_hif4(q_op, ones, khat, 256)[0, 0]) == 1.392578125
 
 
 def test_scores_on_quantized_operands_match_exact_rounding():
-    """On real quantized rows the oracle's scores equal the exact-rational
-    evaluation of the same recipe (every rounding from its definition)."""
+    """On real quantized rows the oracle's scores equal an exact-rational
+    evaluation from the dequantized values themselves (the oracle works from
+    the operand values and the bases instead): each group term summed
+    exactly from the dequantized Q^ and K^ elements, fp32 sums in group
+    order, one fp32 multiply by c, fp16."""
     from fractions import Fraction
     q, k, v, cu = small_case(heads_q=1, heads_kv=1, seqlens=(6,), seed=17, head_dim=128)
     qf = attention.quantize_rows(q[:, 0])
+    qhat = qf["xhat"].reshape(6, 128)
     khat = attention.quantize_rows(k[:, 0])["xhat"].reshape(6, 128)
     q_op = attention.unit_operands(qf).reshape(6, 128)
     s2 = attention.scores_hif4(q_op, qf["scale"], khat, 128)
@@ -286,11 +307,26 @@ def test_scores_on_quantized_operands_match_exact_rounding():
         for j in range(6):
             acc = None
             for g in range(2):
-                dg = sum(Fraction(float(a)) * Fraction(float(b))
-                         for a, b in zip(q_op[i, 64 * g:64 * g + 64], khat[j, 64 * g:64 * g + 64]))
-                wg = _rn32(Fraction(float(qf["scale"][i, g])) / 4 * c)
-                acc = _rn32(dg * wg) if acc is None else _rn32(dg * wg + acc)
-            assert Fraction(float(s2[i, j])) == _rn16(acc), (i, j)
+                tg = sum(Fraction(float(a)) * Fraction(float(b))
+                         for a, b in zip(qhat[i, 64 * g:64 * g + 64], khat[j, 64 * g:64 * g + 64]))
+                acc = tg if acc is None else _rn32(acc + tg)
+            assert Fraction(float(s2[i, j])) == _rn16(_rn32(acc * c)), (i, j)
+
+
+@pytest.mark.parametrize("d", [64, 128, 256])
+def test_scores_within_one_fp16_step_of_exact(d):
+    """Against brute force: S2 is within one fp16 step of the real-number
+    score (dequantized Q^ . dequantized K^) * log2(e)/sqrt(D); a transposed
+    operand, a dropped group, a wrong base or a wrong scale is far outside."""
+    q, k, v, cu = small_case(heads_q=1, heads_kv=1, seqlens=(40,), seed=23, head_dim=d)
+    qf = attention.quantize_rows(q[:, 0])
+    qhat = qf["xhat"].reshape(40, d)
+    khat = attention.quantize_rows(k[:, 0])["xhat"].reshape(40, d)
+    s2 = attention.scores_hif4(attention.unit_operands(qf).reshape(40, d), qf["scale"], khat, d).astype(np.float64)
+    ref = qhat @ khat.T * (math.log2(math.e) / math.sqrt(d))
+    step = np.exp2(np.floor(np.log2(np.maximum(np.abs(ref), 2.0 ** -14))) - 10)
+    assert np.all(np.abs(s2 - ref) <= step)
+    assert np.abs(s2 - ref).max() > 0                 # the scores are rounded, not exact
 
 
 def test_p_only_theorem1_and_constant_v():

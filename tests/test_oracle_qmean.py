@@ -8,6 +8,8 @@ correction; Section 4.6; Appendix C).
     2^-13 is 2048 + 2^-7 (sequential fp32 additions would stay at 2048);
   * constant rows have mean equal to the constant and a zero Q_z; a shift of
     every query element by a constant leaves the Q_z codes unchanged;
+  * the correction mu*kappa is added to the fp32 score accumulator after the
+    group terms with one rounding, and scaled with the rest of the score;
   * with exact arithmetic the corrected scores equal the uncorrected ones,
     so the forward equals brute-force softmax attention;
   * on queries with a DC bias (the case Q-Mean exists for), the quantized
@@ -54,31 +56,38 @@ def test_key_sum_is_exact_before_rounding():
     assert float(kap[0]) == 2048.0 + 2.0 ** -7
 
 
-def test_correction_product_rounds_once_to_fp32():
+def test_correction_product_is_added_with_one_rounding():
+    """fp32(acc + mu*kappa): the exact product enters the sum.  mu = 1 + 2^-10,
+    kappa = 1 + 2^-23, acc = -1: the exact result 2^-10 + 2^-23 + 2^-33 is
+    representable up to the last term (one rounding keeps 2^-23), while
+    rounding the product first loses it."""
     mu = np.array([np.float16(1.0 + 2.0 ** -10)], np.float16)
     kap = np.array([np.float32(1.0 + 2.0 ** -23)], np.float32)
-    # exact product 1 + 2^-10 + 2^-23 + 2^-33 rounds to 1 + 2^-10 + 2^-23
-    c = qmean.correction(mu, kap, np.float32(1.0))
-    assert c.dtype == np.float32
-    assert float(c[0, 0]) == 1.0 + 2.0 ** -10 + 2.0 ** -23
+    acc = np.array([[np.float32(-1.0)]], np.float32)
+    got = qmean.add_correction(acc, mu, kap)
+    assert got.dtype == np.float32
+    assert float(got[0, 0]) == 2.0 ** -10 + 2.0 ** -23 + 2.0 ** -33
+    assert float(np.float32(np.float32(float(mu[0]) * float(kap[0])) - 1.0)) == 2.0 ** -10 + 2.0 ** -23
 
 
-def test_correction_scales_the_mean_first():
-    """corr = fp32(fp32(mu*c) * kappa): mu*c is rounded to fp32 before the
-    product with kappa.  Witness (D = 128, c = fp32(log2(e)/sqrt(128))):
-    mu = -0.496826171875, kappa = 12.613357543945312 gives
-    -0.7991066575050354; one rounding of the exact triple product would give
-    -0.7991065979003906."""
+def test_correction_follows_the_group_terms_and_takes_the_scale():
+    """S2 = fp16(fp32(fp32(fp32(t0 + t1) + mu*kappa) * c)): the correction is
+    added after the group terms, before the scale.  Witness (D = 128):
+    t = (0.7456512451171875, 14.5777587890625), mu = -2.99609375,
+    kappa = -38.7888298034668 give 16.765625; adding a rounded product, or
+    adding the correction before the group terms, gives 16.78125."""
     from fractions import Fraction
-    from tests.test_oracle_attention import _rn32
-    from oracle.attention import score_scale
-    mu = np.array([np.float16(-0.496826171875)], np.float16)
-    kap = np.array([np.float32(12.613357543945312)], np.float32)
-    c = score_scale(128)
-    got = Fraction(float(qmean.correction(mu, kap, c)[0, 0]))
-    f_mu, f_c, f_k = Fraction(float(mu[0])), Fraction(float(c)), Fraction(float(kap[0]))
-    assert got == _rn32(_rn32(f_mu * f_c) * f_k) == Fraction(-0.7991066575050354)
-    assert _rn32(f_mu * f_c * f_k) == Fraction(-0.7991065979003906)
+    from tests.test_oracle_attention import _one_term, _rn16, _rn32
+    t0, t1, mu, kap = 0.7456512451171875, 14.5777587890625, -2.99609375, -38.7888298034668
+    c = Fraction(float(attention.score_scale(128)))
+    f0, f1, fm, fk = Fraction(t0), Fraction(t1), Fraction(mu), Fraction(float(np.float32(kap)))
+    assert _rn16(_rn32(_rn32(_rn32(f0 + f1) + fm * fk) * c)) == Fraction(16.765625)
+    assert _rn16(_rn32(_rn32(_rn32(f0 + f1) + _rn32(fm * fk)) * c)) == Fraction(16.78125)
+    assert _rn16(_rn32(_rn32(_rn32(fm * fk + f0) + f1) * c)) == Fraction(16.78125)
+    q_op, khat = _one_term([t0, t1], 128)
+    s2 = attention.scores_hif4(q_op, np.array([[4.0, 4.0]]), khat, 128,
+                               corr=(np.array([mu], np.float16), np.array([kap], np.float32)))
+    assert float(s2[0, 0]) == 16.765625
 
 
 def test_dc_shift_leaves_q_codes_unchanged():
@@ -115,8 +124,9 @@ def test_q_mean_removes_the_dc_bias_error(monkeypatch):
         e_plain, e_qm = _rel(plain[key]["o"], ex[key]["o"]), _rel(qm[key]["o"], ex[key]["o"])
         assert e_qm < 0.2 and e_qm < 0.7 * e_plain, (key, e_qm, e_plain)
     # the same check fails for a planted sign or scale mistake in the correction
-    good = attention.correction
-    for bad in (lambda mu, ka, c: -good(mu, ka, c), lambda mu, ka, c: good(mu, ka, c) * np.float32(0.5)):
-        monkeypatch.setattr(attention, "correction", bad)
+    good = qmean.add_correction
+    for bad in (lambda acc, mu, ka: good(acc, -mu, ka),
+                lambda acc, mu, ka: good(acc, mu, ka * np.float32(0.5))):
+        monkeypatch.setattr(qmean, "add_correction", bad)
         wrong = attention.attention_fwd(q, k, v, None, cu_seqlens=cu, q_mean=True)
         assert min(_rel(wrong[key]["o"], ex[key]["o"]) for key in ex) > 0.3
