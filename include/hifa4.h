@@ -130,9 +130,12 @@ typedef enum {
  *                  Appendix C).  Per query row mu = fp16(exact sum of the
  *                  row's D smoothed values / D); the row is quantized as
  *                  Q_z = fp16(q~ - mu); per key kappa = fp32(exact sum of the
- *                  key's smoothed channels); the score accumulator starts from
- *                  fp32(fp32(mu*c) * kappa).  HIF4 operands only
- *                  (HIFA4_ERR_UNSUPPORTED with FP16 operands). */
+ *                  key's smoothed channels); after the group terms the score
+ *                  accumulator takes fp32(S_acc + mu*kappa) (the exact
+ *                  product added with one rounding), before the multiply by
+ *                  c.  HIF4 operands only (HIFA4_ERR_UNSUPPORTED with FP16
+ *                  operands).
+ *   test_decode_no_publish  testing only; see hifa4_decode_fwd (0 otherwise). */
 typedef struct {
   int32_t norm;       /* hifa4_norm      */
   int32_t operands;   /* hifa4_operands  */
@@ -200,10 +203,10 @@ hifa4_status hifa4_calibrate_smooth_qk_layers(const hifa4_problem* p, int32_t n_
                                               hifa4_calib_report* reports, void* workspace,
                                               size_t workspace_bytes, void* stream);
 
-/* Smooth-QK then HIF4 quantization of Q~ = fp16(fp32(q)*s) and
- * K~ = fp16(fp32(k)/s) (IEEE single multiply / correctly rounded divide, one
- * rounding to fp16), in groups of 64 consecutive channels of each (token,
- * head) row (Algorithm 1, the Smooth-QK and HIF4 steps).
+/* Smooth-QK then HIF4 quantization of Q~ = fp16(q*s) and K~ = fp16(k/s),
+ * each the exact product or quotient of the fp16 input and the fp32 scale
+ * rounded once to fp16 (nearest even), in groups of 64 consecutive channels
+ * of each (token, head) row (Algorithm 1, the Smooth-QK and HIF4 steps).
  * q, k: DEVICE fp16 in the problem's layout; s: DEVICE fp32
  * [num_heads_kv, head_dim] or NULL (no smoothing).
  * Outputs (DEVICE, canonical layout):
@@ -232,12 +235,11 @@ hifa4_status hifa4_quantize_v(const hifa4_problem* p, const void* v, void* v_cod
  * q: DEVICE fp16 [.., num_heads_q, head_dim]; k, v: DEVICE fp16
  * [.., num_heads_kv, head_dim]; s: DEVICE fp32 [num_heads_kv, head_dim] (may be
  * NULL when opt->smooth_qk == 0 or operands are FP16).
- * Per query row and 64-key block in ascending order: with c =
- * fp32(log2(e)/sqrt(D)) and, per 64-channel group g of the query, its E6M2
- * base b_g and weight w_g = fp32(b_g/4 * c), the exact group dot d_g of the
- * query's operand values (+-u*2^-sh) with the dequantized keys is
- * accumulated in fp32 as acc = fp32(d_0*w_0) (with Q-Mean: the fused d_0*w_0
- * + the correction), then acc = fp32(d_g*w_g + acc) fused, and S2 = fp16(acc);
+ * Per query row and 64-key block in ascending order, with c =
+ * fp32(log2(e)/sqrt(D)): per 64-channel group g the exact term t_g = the dot
+ * of the dequantized Q^ and K^ groups; S_acc = the fp32 sum of the t_g in
+ * group order, each addition rounded once (with Q-Mean, then
+ * fp32(S_acc + mu*kappa)); S2 = fp16(fp32(S_acc * c));
  * m_new = max(m, rowmax S2); P = fp16(2^(S2-m_new));
  * r = fp16(2^(m-m_new)); P^ = HIF4(P); O = r*O + P^ V^ and l = r*l + P^ 1
  * (fp32 accumulation); O_out = fp16(O/l), LSE = m*ln2 + ln(l).

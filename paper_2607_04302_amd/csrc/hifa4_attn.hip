@@ -15,9 +15,9 @@
 //   S^T[key, q] = K^ Q^T with two 32x32x64 FP6 MFMAs per 64-channel group
 //     and 32-key half (the A operands are the pre-pass K records in LDS, whose
 //     E8M0 scales carry b_K exactly; B is the Q tile quantized in registers at
-//     kernel start); each group sum is exact, the fp32 epilogue applies
-//     fp32(b_Q/4 * c) per group (c the softmax scale) and accumulates the
-//     groups in order with fused multiply-adds, then rounds to fp16.  In S^T
+//     kernel start); each group sum is exact, the fp32 epilogue forms each
+//     group's exact term (times b_Q/4), sums the groups in order in fp32,
+//     multiplies by the score scale c in fp32 and rounds to fp16.  In S^T
 //     each lane holds one query and 32 of the block's keys, so row maxima are
 //     in-lane plus one exchange with lane l^32;
 //   FP16 softmax: m_new = max(m, rowmax), P = 2^(S2 - m_new), r = 2^(m - m_new);
@@ -165,10 +165,11 @@ __device__ __forceinline__ int key_of(int t, int h, int v) { return 32 * t + 8 *
 // negated codes), with E8M0 row scales that together make K's exact b/4; the
 // result is the exact sum of o_q * (o_k * b_k/4) in fp32.  V^ enters the PV
 // product the same way, so its groups are exact too.  The epilogue
-// multiplies by the lane's own w_g = fp32(b_q/4 * c) (each lane owns one query
-// in S^T; the softmax scale c is folded in) and accumulates the groups in
-// order with fused multiply-adds: G VALU operations per score plus the fp16
-// rounding.
+// multiplies by the lane's own b_q/4 (each lane owns one query in S^T), which
+// gives the group's exact term t_g; the terms are summed in order in fp32 (a
+// fused multiply-add of the exact product rounds exactly the sum), the sum
+// is multiplied by c, then rounded to fp16: G + 1 VALU operations per score
+// plus the fp16 rounding.
 //
 // Deferred rescale: instead of O <- r*O every block, the kernel keeps
 // O* = O / rho and l* = l / rho with rho the product of the rescale factors so
@@ -286,9 +287,9 @@ __device__ __forceinline__ void smooth_half_group(const QRaw& r, bool smooth, h2
 // Q-Mean (Algorithm 1, the mean step): mu = fp16(sum of the row's D smoothed
 // values / D), the sum exact in float64, then Q_z = fp16(q~ - mu) in place
 // (one packed fp16 subtraction per pair, each difference rounded once).
-// The lane pair (l, l^32) holds the row; returns fp32(mu * c).
+// The lane pair (l, l^32) holds the row; returns mu as fp32 (exact).
 template <int G>
-__device__ __forceinline__ float centre_q_row(h2_t (&x)[G][16], float c) {
+__device__ __forceinline__ float centre_q_row(h2_t (&x)[G][16]) {
   double part = 0.0;
 #pragma unroll
   for (int g = 0; g < G; ++g)
@@ -301,18 +302,19 @@ __device__ __forceinline__ float centre_q_row(h2_t (&x)[G][16], float c) {
   for (int g = 0; g < G; ++g)
 #pragma unroll
     for (int i = 0; i < 16; ++i) x[g][i] = x[g][i] - mu2;
-  return (float)mu * c;
+  return (float)mu;
 }
 
 // HIF4 of one query group (row layout, see rows_quantize): the lane's FP6 B
-// operand and the group's fp32 score weight w = fp32(b/4 * c).
-__device__ __forceinline__ void quantize_q_half_group(const h2_t (&x)[16], float c, i8_t& qop, float& wq) {
+// operand and the group's scale b/4 (exact), which turns the MFMA's group
+// dot into the group's exact score term.
+__device__ __forceinline__ void quantize_q_half_group(const h2_t (&x)[16], i8_t& qop, float& wq) {
   const GroupOps r = rows_quantize(x);
 #pragma unroll
   for (int i = 0; i < 6; ++i) qop[i] = r.pk[i];
   qop[6] = 0;
   qop[7] = 0;
-  wq = (0.25f * r.bval) * c;      // b/4 exact, one rounding with c
+  wq = 0.25f * r.bval;
 }
 
 template <int G>
@@ -331,8 +333,10 @@ __device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm,
   constexpr int DT = 2 * G;
   constexpr ChunkLayout lay = chunk_layout_hif4(G, QMEAN);
   constexpr int CB = (int)lay.bytes;
-  // ---- scores: S2 = fp16(acc), acc = fp32(d_0 w_0) then fused d_g w_g + acc,
-  // with w_g = fp32(b_q,g/4 * c) (the softmax scale folded into the group scale).
+  // ---- scores: S2 = fp16(fp32(S_acc * c)), S_acc the fp32 sum of the exact
+  // group terms t_g = d_g * b_q,g/4 in group order (with Q-Mean, then
+  // fp32(S_acc + mu kappa_j)); a fused multiply-add of an exact product
+  // rounds exactly the sum.
   h2_t s2[2][8];
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
@@ -353,27 +357,29 @@ __device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm,
     stream_piece<CB>(cs, 2 + t);
     float sacc[16];
     if (QMEAN) {
-      // the accumulator starts from the Q-Mean correction fp32(fp32(mu c) kappa_j)
-      // of the lane's keys 32t + 8j + 4h + [0, 4), four keys at a time so that
-      // the corrections occupy no more registers than the dying accumulators
+      // the Q-Mean correction mu * kappa_j of the lane's keys 32t + 8j + 4h +
+      // [0, 4) follows the group terms, four keys at a time so that the key
+      // sums occupy no more registers than the dying accumulators
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const float4 kp = *reinterpret_cast<const float4*>(cur + lay.kappa + 4 * (32 * t + 8 * j + 4 * h));
         const float kv[4] = {kp.x, kp.y, kp.z, kp.w};
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          float x = cmu * kv[i];
+          float x = acc[0][4 * j + i] * wq[0];
 #pragma unroll
-          for (int g = 0; g < G; ++g) x = __builtin_fmaf(acc[g][4 * j + i], wq[g], x);
-          sacc[4 * j + i] = x;
+          for (int g = 1; g < G; ++g) x = __builtin_fmaf(acc[g][4 * j + i], wq[g], x);
+          x = __builtin_fmaf(cmu, kv[i], x);
+          sacc[4 * j + i] = x * a.c;
         }
       }
     } else {
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        sacc[v] = acc[0][v] * wq[0];
+        float x = acc[0][v] * wq[0];
 #pragma unroll
-        for (int g = 1; g < G; ++g) sacc[v] = __builtin_fmaf(acc[g][v], wq[g], sacc[v]);
+        for (int g = 1; g < G; ++g) x = __builtin_fmaf(acc[g][v], wq[g], x);
+        sacc[v] = x * a.c;
       }
     }
 #pragma unroll
@@ -520,11 +526,11 @@ __global__ void __launch_bounds__(256, (G == 1 ? 4 : (G == 2 ? 3 : 1))) k_attn_h
 #pragma unroll
   for (int g = 0; g < G; ++g) smooth_half_group(raw[g], a.s != nullptr, xs[g]);
   float cmu = 0.0f;
-  if (QMEAN) cmu = centre_q_row<G>(xs, a.c);
+  if (QMEAN) cmu = centre_q_row<G>(xs);
   i8_t qop[G];
   float wq[G];
 #pragma unroll
-  for (int g = 0; g < G; ++g) quantize_q_half_group(xs[g], a.c, qop[g], wq[g]);
+  for (int g = 0; g < G; ++g) quantize_q_half_group(xs[g], qop[g], wq[g]);
 
   i8_t ones;
   {

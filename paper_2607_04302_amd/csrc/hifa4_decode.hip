@@ -200,8 +200,9 @@ struct ScoreLds {
 // are zero), B = 32 keys of the block; per (32-key tile, channel group) the
 // two MFMAs give the exact group dots 16 * sum(q_unit * k_unit) of query rows
 // 4h + c with key (l & 31) of the tile.  Epilogue per group: d_g = dot * b_K/64
-// (exact), acc = fp32(d_0 w_0), then acc = fma(d_g, w_g, acc) with
-// w_g = fp32(b_Q,g/4 * c); S2 = fp16(acc).  Two register buffers in fixed
+// (exact), the group's exact term t_g = d_g * b_Q,g/4, the terms summed in
+// order in fp32 (a fused multiply-add of the exact product rounds exactly the
+// sum), S2 = fp16(fp32(sum * c)).  Two register buffers in fixed
 // roles keep the next two blocks' codes in flight; the scores and maxima of
 // the run are collected in LDS and stored after the last block, so the loop
 // issues loads only.
@@ -258,16 +259,16 @@ __device__ __forceinline__ void score_run(const DecodeArgs& a, const WaveSpan& w
   for (int p = 0; p < kQPasses; ++p) {
     const int pi = 4 * p + (lane >> 4), r = pi / G, g = pi % G;
     if (4 * p >= grp * G) break;                             // uniform: no pair of this pass is live
-    const h2_t x01 = __builtin_bit_cast(h2_t, qraw[p].x), x23 = __builtin_bit_cast(h2_t, qraw[p].y);
-    const float sv[4] = {qs[p].x, qs[p].y, qs[p].z, qs[p].w};
-    const half_t xin[4] = {x01[0], x01[1], x23[0], x23[1]};
+    // q~ = fp16(q * s), the exact product rounded once (mixed-precision fma)
+    const h2_t y01 = smooth_mul2(__builtin_bit_cast(h2_t, qraw[p].x), qs[p].x, qs[p].y);
+    const h2_t y23 = smooth_mul2(__builtin_bit_cast(h2_t, qraw[p].y), qs[p].z, qs[p].w);
+    const half_t xsm[4] = {y01[0], y01[1], y23[0], y23[1]};
     float ax[4];
     bool neg[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const half_t xs = (half_t)((float)xin[j] * sv[j]);
-      ax[j] = fabsf((float)xs);
-      neg[j] = (float)xs < 0.0f;
+      ax[j] = fabsf((float)xsm[j]);
+      neg[j] = (float)xsm[j] < 0.0f;
     }
     const float a4 = fmaxf(fmaxf(ax[0], ax[1]), fmaxf(ax[2], ax[3]));
     const float a8 = fmaxf(a4, __shfl_xor(a4, 1));
@@ -305,7 +306,7 @@ __device__ __forceinline__ void score_run(const DecodeArgs& a, const WaveSpan& w
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       const int r = 4 * h + c;
-      wq[g][c] = (0.25f * e6m2_value(sl.qb[wave][(r < grp ? r : 0) * G + g])) * a.c;
+      wq[g][c] = 0.25f * e6m2_value(sl.qb[wave][(r < grp ? r : 0) * G + g]);
     }
   }
   load(min(J0 + 1, J1 - 1), b1);
@@ -334,7 +335,7 @@ __device__ __forceinline__ void score_run(const DecodeArgs& a, const WaveSpan& w
       float m = -__builtin_inff();
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
-        sv[t] = 64 * J + 32 * t + n < L ? (half_t)acc[t][c] : (half_t)(-__builtin_inff());
+        sv[t] = 64 * J + 32 * t + n < L ? (half_t)(acc[t][c] * a.c) : (half_t)(-__builtin_inff());
         m = fmaxf(m, (float)sv[t]);
       }
 #pragma unroll
