@@ -112,14 +112,20 @@ typedef enum {
 
 /* Options of hifa4_attention_fwd.
  *   smooth_qk      0: the scale vector is ignored (treated as all ones);
- *   debug_p_codes  NULL, or a DEVICE uint8 buffer [num_heads_q, T, NB, 32]
- *                  receiving the canonical codes of every P^ group, where T
- *                  is the token count (BSHD: batch*max_seqlen) and
- *                  NB = ceil(max_seqlen/64); entry (h, t, J) is written for
- *                  the 64-key blocks J <= i/64 that query t (position i in
- *                  its sequence) sees, other entries are left untouched;
- *   debug_p_meta   NULL, or a DEVICE uint32 buffer [num_heads_q, T, NB] with
- *                  the matching metadata words.  Both or neither.
+ *   debug_p_codes  NULL, or a DEVICE uint8 buffer [NH, NT, NB, 32]
+ *                  receiving the canonical codes of the P^ groups of query
+ *                  heads [h0, h0+NH) and tokens [t0, t0+NT) (the dump window,
+ *                  below), NB = ceil(max_seqlen/64); entry (h-h0, t-t0, J) is
+ *                  written for the 64-key blocks J <= i/64 that query t
+ *                  (position i in its sequence) sees, other entries are left
+ *                  untouched;
+ *   debug_p_meta   NULL, or a DEVICE uint32 buffer [NH, NT, NB] with the
+ *                  matching metadata words.  Both or neither.
+ *   debug_head_begin/_count, debug_token_begin/_count  the dump window
+ *                  h0, NH, t0, NT; a count of 0 means every query head
+ *                  (every token, T = batch*max_seqlen for BSHD) and needs a
+ *                  begin of 0; a window outside the problem fails with
+ *                  HIFA4_ERR_INVALID_ARGUMENT.
  * Debug dumps are produced for HIFA4_OPERANDS_HIF4 and _P_ONLY.
  *   timing_events  NULL, or a HOST array of three hipEvent_t (created by the
  *                  caller) that the call records on `stream` before the K/V
@@ -145,6 +151,10 @@ typedef struct {
   void** timing_events;
   int32_t q_mean;
   int32_t test_decode_no_publish;  /* testing only, hifa4_decode_fwd: see there */
+  int32_t debug_head_begin;        /* P^ dump window of hifa4_attention_fwd */
+  int32_t debug_head_count;
+  int32_t debug_token_begin;
+  int32_t debug_token_count;
 } hifa4_fwd_options;
 
 /* Host-side calibration report (Table 1 statistics and the gate decision). */

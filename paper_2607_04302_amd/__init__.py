@@ -43,7 +43,9 @@ class FwdOptions(ctypes.Structure):
     _fields_ = [("norm", ctypes.c_int32), ("operands", ctypes.c_int32), ("smooth_qk", ctypes.c_int32),
                 ("debug_p_codes", ctypes.c_void_p), ("debug_p_meta", ctypes.c_void_p),
                 ("timing_events", ctypes.c_void_p), ("q_mean", ctypes.c_int32),
-                ("test_decode_no_publish", ctypes.c_int32)]
+                ("test_decode_no_publish", ctypes.c_int32),
+                ("debug_head_begin", ctypes.c_int32), ("debug_head_count", ctypes.c_int32),
+                ("debug_token_begin", ctypes.c_int32), ("debug_token_count", ctypes.c_int32)]
 
 
 class CalibReport(ctypes.Structure):
@@ -274,12 +276,13 @@ _default_ws = Workspace()
 def hifa4_attention_fwd(q, k, v, s=None, cu_seqlens=None, max_seqlen=None, norm: int = NORM_PREORDER,
                         operands: int = OPERANDS_HIF4, smooth_qk: Optional[bool] = None, debug_p: bool = False,
                         out=None, lse=None, workspace: Optional[Workspace] = None, timing_events=None,
-                        q_mean: bool = False):
+                        q_mean: bool = False, debug_heads=None, debug_tokens=None):
     """HiFA4 causal prefill forward.  Returns (o, lse) or, with debug_p,
-    (o, lse, p_codes uint8 [Hq,T,NB,32], p_meta int32 [Hq,T,NB]).
-    timing_events: optional three recorded torch.cuda.Event objects (before
-    the pre-pass, before the attention kernel, after it).  q_mean: the Q-Mean
-    auxiliary (HIF4 operands only)."""
+    (o, lse, p_codes uint8 [NH,NT,NB,32], p_meta int32 [NH,NT,NB]) for the
+    dump window debug_heads = (h0, NH) and debug_tokens = (t0, NT) (default:
+    every head and token).  timing_events: optional three recorded
+    torch.cuda.Event objects (before the pre-pass, before the attention
+    kernel, after it).  q_mean: the Q-Mean auxiliary (HIF4 operands only)."""
     torch = _torch()
     for t, n in ((q, "q"), (k, "k"), (v, "v")):
         _require(t, torch.float16, n)
@@ -292,15 +295,18 @@ def hifa4_attention_fwd(q, k, v, s=None, cu_seqlens=None, max_seqlen=None, norm:
     o = torch.empty_like(q) if out is None else out
     l = torch.empty((sh.heads_q, sh.tokens), dtype=torch.float32, device=dev) if lse is None else lse
     pc = pm = None
+    h0, nh = debug_heads if debug_heads is not None else (0, 0)
+    t0, nt = debug_tokens if debug_tokens is not None else (0, 0)
     if debug_p:
         nb = (sh.max_seqlen + 63) // 64
-        pc = torch.zeros((sh.heads_q, sh.tokens, nb, 32), dtype=torch.uint8, device=dev)
-        pm = torch.zeros((sh.heads_q, sh.tokens, nb), dtype=torch.int32, device=dev)
+        pc = torch.zeros((nh or sh.heads_q, nt or sh.tokens, nb, 32), dtype=torch.uint8, device=dev)
+        pm = torch.zeros((nh or sh.heads_q, nt or sh.tokens, nb), dtype=torch.int32, device=dev)
     ev_arr = None
     if timing_events is not None:
         ev_arr = (ctypes.c_void_p * 3)(*[e.cuda_event for e in timing_events])
     opt = FwdOptions(norm, operands, 1 if smooth_qk else 0, _ptr(pc), _ptr(pm),
-                     ctypes.cast(ev_arr, ctypes.c_void_p) if ev_arr is not None else None, 1 if q_mean else 0)
+                     ctypes.cast(ev_arr, ctypes.c_void_p) if ev_arr is not None else None, 1 if q_mean else 0,
+                     0, h0, nh, t0, nt)
     p = sh.problem()
     need = int(lib.hifa4_workspace_bytes(ctypes.byref(p), ctypes.byref(opt)))
     ws = (workspace or _default_ws).get(need, dev)

@@ -151,6 +151,12 @@ hifa4_status hifa4_attention_fwd(const hifa4_problem* p, const hifa4_fwd_options
     return fail(HIFA4_ERR_INVALID_ARGUMENT, "debug_p_codes and debug_p_meta must both be set or both be NULL");
   if ((st = check_aligned16({q, k, v, o, s, workspace, opt->debug_p_codes})) != HIFA4_OK) return st;
   if ((st = check_aligned4({lse, p->cu_seqlens, opt->debug_p_meta})) != HIFA4_OK) return st;
+  if (opt->debug_head_count < 0 || opt->debug_token_count < 0 || opt->debug_head_begin < 0 ||
+      opt->debug_token_begin < 0 || (!opt->debug_head_count && opt->debug_head_begin) ||
+      (!opt->debug_token_count && opt->debug_token_begin) ||
+      (long)opt->debug_head_begin + opt->debug_head_count > p->num_heads_q ||
+      (long)opt->debug_token_begin + opt->debug_token_count > (long)d.tokens)
+    return fail(HIFA4_ERR_INVALID_ARGUMENT, "debug window outside the problem");
   // FP16 and P-only keep Q, K and V in fp16 (fp16 chunk layout, no smoothing)
   const bool fp16 = opt->operands != HIFA4_OPERANDS_HIF4;
   if (fp16 && opt->q_mean)
@@ -180,6 +186,10 @@ hifa4_status hifa4_attention_fwd(const hifa4_problem* p, const hifa4_fwd_options
   const bool dump = opt->operands != HIFA4_OPERANDS_FP16;
   a.dbg_codes = dump ? (uint8_t*)opt->debug_p_codes : nullptr;
   a.dbg_meta = dump ? (uint32_t*)opt->debug_p_meta : nullptr;
+  a.dbg_h0 = opt->debug_head_count ? opt->debug_head_begin : 0;
+  a.dbg_nh = opt->debug_head_count ? opt->debug_head_count : p->num_heads_q;
+  a.dbg_t0 = opt->debug_token_count ? opt->debug_token_begin : 0;
+  a.dbg_nt = opt->debug_token_count ? opt->debug_token_count : (int)d.tokens;
   a.batch = p->batch;
   a.S = d.S;
   a.NB = d.NB;

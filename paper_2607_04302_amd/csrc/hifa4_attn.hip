@@ -428,8 +428,8 @@ __device__ __forceinline__ void hif4_block(const AttnArgs& a, const TileMap& tm,
   // ---- P^ = HIF4(P) over the block's 64 keys (P-Reordering).
   uint8_t* dcodes = nullptr;
   uint32_t* dmeta = nullptr;
-  if (DEBUG && row_ok) {
-    const size_t e = ((size_t)tm.hq * a.total_tokens + tm.t0 + qi) * a.NB + J;
+  size_t e;
+  if (DEBUG && row_ok && dbg_entry(a, tm.hq, tm.t0 + qi, J, e)) {
     dcodes = a.dbg_codes + e * 32;
     dmeta = a.dbg_meta + e;
   }
@@ -845,8 +845,8 @@ __global__ void __launch_bounds__(256, (D <= 128 ? 2 : 1)) k_attn_ponly(AttnArgs
       stream_piece<cbytes>(cs, 3);
       uint8_t* dcodes = nullptr;
       uint32_t* dmeta = nullptr;
-      if (DEBUG && row_ok) {
-        const size_t e = ((size_t)tm.hq * a.total_tokens + tm.t0 + qi) * a.NB + J;
+      size_t e;
+      if (DEBUG && row_ok && dbg_entry(a, tm.hq, tm.t0 + qi, J, e)) {
         dcodes = a.dbg_codes + e * 32;
         dmeta = a.dbg_meta + e;
       }

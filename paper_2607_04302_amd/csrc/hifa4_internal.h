@@ -60,11 +60,22 @@ struct AttnArgs {
   const uint8_t* ws;       // pre-pass chunks
   half_t* o;
   float* lse;
-  uint8_t* dbg_codes;      // optional P^ dump
-  uint32_t* dbg_meta;
+  uint8_t* dbg_codes;      // optional P^ dump [dbg_nh, dbg_nt, NB, 32]
+  uint32_t* dbg_meta;      // [dbg_nh, dbg_nt, NB]
+  int dbg_h0, dbg_nh;      // dumped query heads [dbg_h0, dbg_h0 + dbg_nh)
+  int dbg_t0, dbg_nt;      // dumped tokens [dbg_t0, dbg_t0 + dbg_nt)
   int batch, S, NB, hq, hkv, D, total_tokens;
   float c;                 // log2(e)/sqrt(D)
 };
+
+// Entry of the P^ dump for (query head, token, block), false outside the
+// dumped window.
+__device__ __forceinline__ bool dbg_entry(const AttnArgs& a, int hq, int tok, int J, size_t& e) {
+  const int hr = hq - a.dbg_h0, tr = tok - a.dbg_t0;
+  if ((unsigned)hr >= (unsigned)a.dbg_nh || (unsigned)tr >= (unsigned)a.dbg_nt) return false;
+  e = ((size_t)hr * a.dbg_nt + tr) * a.NB + J;
+  return true;
+}
 
 hipError_t launch_quant_rows(const half_t* x, const float* s, uint8_t* codes, uint32_t* meta, long n_rows,
                              int heads, int heads_kv, int D, bool is_k, hipStream_t st);

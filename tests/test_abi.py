@@ -62,6 +62,12 @@ def test_validation_codes(lib):
     assert "q_mean" in h.hifa4_last_error()
     assert _fwd(lib, _p(), ws=16) == -3
     assert "workspace" in h.hifa4_last_error()
+    # P^ dump windows: outside the problem, negative, or a begin without a count
+    tokens = _p().batch * _p().max_seqlen
+    for win in ((0, _p().num_heads_q + 1, 0, 0), (1, _p().num_heads_q, 0, 0), (0, 0, 0, tokens + 1),
+                (-1, 1, 0, 0), (0, 0, 5, 0), (0, 0, tokens - 1, 2), (0, -1, 0, 0)):
+        assert _fwd(lib, _p(), opt=h.FwdOptions(0, 0, 0, FAKE, FAKE, None, 0, 0, *win)) == -1, win
+        assert "debug window" in h.hifa4_last_error()
     assert lib.hifa4_selftest_exp2(None, None, -1, None) == -1
 
 

@@ -343,3 +343,26 @@ def test_decode_wait_gives_up(h):
     assert torch.isnan(o).all() and torch.isnan(l).all(), "a wait that gave up must poison its row"
     _say("decode give-up rows are NaN")
     _decode_and_compare(h, qd, k, v, cu, s, max(lens), seqs=[1, 7], kv_heads=[0, 1])
+
+
+@pytest.mark.parametrize("kind,jump_block,lens", [
+    ("wipe", 2, (450, 200)),          # the jump opens the second split: the merge wipes the first
+    ("wipe", 1, (450, 200)),          # the jump inside the first split
+    ("renorm", 0, (450, 400)),
+    ("wipe", 2, (4096,) * 8),         # fused shape (256 split workgroups)
+    ("renorm", 0, (4096,) * 8),
+])
+def test_decode_running_max_special_paths(h, kind, jump_block, lens):
+    """The decode row (L-1) of inputs whose running maximum jumps by more
+    than 25 log2 units (a rescale factor of 0, so earlier blocks or splits
+    are wiped) or rises over 64 units in smaller steps: every P^ code of the
+    sampled rows bit-exact, O and LSE, both normalizers."""
+    from _jump import check_jumps, jump_case
+    d, hq, hkv = 128, 4, 1
+    q, k, v, cu = jump_case(kind, lens, hq, hkv, d, seed=81, jump_block=jump_block)
+    check_jumps(kind, q, k, cu, d, "hif4", last_row_only=True, min_hits=len(lens))
+    qd = _last_queries(q, cu)
+    seqs = None if len(lens) <= 2 else [0, 5]
+    for norm in ("preorder", "inconsistent"):
+        _say("decode running max", kind, jump_block, len(lens), norm)
+        _decode_and_compare(h, qd, k, v, cu, None, max(lens), norm=norm, seqs=seqs)

@@ -15,6 +15,7 @@ from oracle.softmax16 import exp2_fp16
 from paper_2607_04302_amd.workloads import WORKLOADS, make_calibration, make_inputs, small_case
 
 from _edge import edge_rows, edge_tokens
+from _jump import check_jumps, jump_case
 from _gpu_util import check_close, to_gpu, to_np
 
 pytestmark = pytest.mark.gpu
@@ -114,16 +115,29 @@ def test_quantize_v_bitexact(h):
 
 
 def _run_and_compare(h, q, k, v, cu, s, max_seqlen, norm="preorder", heads=None, rows=None, check_p=True,
-                     seqs=None, q_mean=False):
+                     seqs=None, q_mean=False, dump_per_head=False):
     """Runs the HIP forward on the whole problem, the oracle on the sampled
     (sequence, head, row) set, and compares O, LSE and (check_p) the P^ dump.
-    Only the sampled slices of the GPU outputs are copied to the host."""
+    Only the sampled slices of the GPU outputs are copied to the host.
+    dump_per_head: the P^ dump is taken head by head (a dump window of one
+    query head, one more forward per sampled head), for problems whose whole
+    dump would not fit."""
     import torch
     cu_t = None if cu is None else to_gpu(cu)
     nm = h.NORM_PREORDER if norm == "preorder" else h.NORM_INCONSISTENT
-    res = h.hifa4_attention_fwd(to_gpu(q), to_gpu(k), to_gpu(v), None if s is None else to_gpu(s),
-                                cu_seqlens=cu_t, max_seqlen=max_seqlen, norm=nm, debug_p=check_p, q_mean=q_mean)
+    args = (to_gpu(q), to_gpu(k), to_gpu(v), None if s is None else to_gpu(s))
+    res = h.hifa4_attention_fwd(*args, cu_seqlens=cu_t, max_seqlen=max_seqlen, norm=nm,
+                                debug_p=check_p and not dump_per_head, q_mean=q_mean)
     o, lse = res[0], res[1]
+    dumps = {}
+    if check_p and dump_per_head:
+        for hh in heads:
+            r1 = h.hifa4_attention_fwd(*args, cu_seqlens=cu_t, max_seqlen=max_seqlen, norm=nm, debug_p=True,
+                                       q_mean=q_mean, debug_heads=(hh, 1))
+            dumps[hh] = (r1[2][0], r1[3][0])
+            torch.cuda.synchronize()
+    elif check_p:
+        dumps = {hh: (res[2][hh], res[3][hh]) for hh in range(q.shape[-2])}
     ref = oatt.attention_fwd(q, k, v, s, cu_seqlens=cu, norm=norm, heads=heads, rows=rows, want_p=check_p,
                              seqs=seqs, q_mean=q_mean)
     if cu is None:
@@ -141,8 +155,8 @@ def _run_and_compare(h, q, k, v, cu, s, max_seqlen, norm="preorder", heads=None,
         worst = max(worst, check_close(to_np(o[tok_t, hh]), r["o"], what=f"O seq {b} head {hh}"))
         check_close(to_np(lse[hh, tok_t]), r["lse"], atol=2e-3, rtol=0, what="LSE")
         if check_p:
-            pc = to_np(res[2][hh, tok_t])
-            pm = to_np(res[3][hh, tok_t]).view(np.uint32)
+            pc = to_np(dumps[hh][0][tok_t])
+            pm = to_np(dumps[hh][1][tok_t]).view(np.uint32)
             for ii, i in enumerate(r["rows"]):
                 nb_i = i // 64 + 1
                 assert np.array_equal(pc[ii, :nb_i], r["p_codes"][ii, :nb_i]), (b, hh, i)
@@ -263,16 +277,16 @@ def test_qwen3_shape_sampled(h):
 def test_long_s32768_sampled(h):
     """Long prefill, S=32768, at full size in the benchmark's launch shape,
     Smooth-QK scales from the Qwen3-shaped calibration draw: sampled heads and
-    rows (first, block edges, middle, last); O and LSE against the oracle.
-    The P^ dump is not requested here (it would take 17 GB at this length);
-    P^ codes are compared bit for bit on the S=4096 workload."""
+    rows (first, block edges, middle, last); every P^ code of those rows bit
+    exact (a dump window of one head at a time: 0.5 GiB instead of 17 GB for
+    every head), O and LSE against the oracle."""
     w = WORKLOADS["long_s32768"]
     q, k, v, _ = make_inputs(w)
     qc, kc = make_calibration(WORKLOADS[w.calib_from], n=4)
     s, _ = osmooth.calibrate(qc, kc, w.heads_kv, w.alpha)
     rows = [0, 63, 64, 4097, 16383, 16384, 32700, 32767]
     _say("long_s32768 sampled")
-    _run_and_compare(h, q, k, v, None, s, w.seqlen, heads=[2, 29], rows=rows, check_p=False)
+    _run_and_compare(h, q, k, v, None, s, w.seqlen, heads=[2, 29], rows=rows, dump_per_head=True)
 
 
 def test_varlen_b16_full(h):
@@ -432,3 +446,45 @@ def test_calibration_layers(h):
         assert abs(reps[i]["t_kq"] - rep["t_kq"]) < 1e-12 * rep["t_kq"]
         branches.append(rep["branch"])
     assert branches == [2, 1, 0]
+
+
+# ---------------------------------------------------------------------------
+# The running maximum's special paths ("P-Reordering under online softmax"):
+# a block whose maximum exceeds the running maximum by more than 25 in log2
+# units makes the rescale factor r = E(fp16(m - m_new)) exactly 0 (the
+# history is wiped), and a maximum that grows in steps below that over more
+# than 64 units drives the product of the rescale factors below 2^-64, where
+# the kernel's deferred rescale renormalizes.  Integer Q and K keep the fp16
+# scores exact on the P-only path too, so P^ is bit-exact there as well.
+
+@pytest.mark.parametrize("kind", ["wipe", "renorm"])
+@pytest.mark.parametrize("d,hq,hkv", [(128, 2, 1), (64, 4, 2)])
+def test_running_max_special_paths(h, kind, d, hq, hkv):
+    lens = (450, 200)
+    q, k, v, cu = jump_case(kind, lens, hq, hkv, d, seed=61 + d)
+    check_jumps(kind, q, k, cu, d, "hif4")
+    for norm in ("preorder", "inconsistent"):
+        _say("running max", kind, d, hq, hkv, norm)
+        _run_and_compare(h, q, k, v, cu, None, max(lens), norm=norm)
+
+
+@pytest.mark.parametrize("kind", ["wipe", "renorm"])
+def test_running_max_special_paths_p_only(h, kind):
+    lens = (450, 130)
+    d, hq, hkv = 128, 2, 1
+    q, k, v, cu = jump_case(kind, lens, hq, hkv, d, seed=71)
+    check_jumps(kind, q, k, cu, d, "p_only")
+    for norm in ("preorder", "inconsistent"):
+        _say("running max p_only", kind, norm)
+        res = _run_ponly(h, q, k, v, cu, max(lens), norm, True)
+        ref = oatt.attention_fwd(q, k, v, None, cu_seqlens=cu, operands="p_only", norm=norm, want_p=True)
+        o, lse = to_np(res[0]), to_np(res[1])
+        pc, pm = to_np(res[2]), to_np(res[3]).view(np.uint32)
+        for (b, hh), r in ref.items():
+            tok = cu[b] + r["rows"]
+            check_close(o[tok, hh], r["o"], what=f"p_only O seq {b} head {hh}")
+            check_close(lse[hh, tok], r["lse"], atol=2e-3, rtol=0, what="p_only LSE")
+            for ii, i in enumerate(r["rows"]):
+                nb_i = i // 64 + 1
+                assert np.array_equal(pc[hh, tok[ii], :nb_i], r["p_codes"][ii, :nb_i]), (b, hh, i)
+                assert np.array_equal(pm[hh, tok[ii], :nb_i], r["p_meta"][ii, :nb_i]), (b, hh, i)
