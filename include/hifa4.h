@@ -262,6 +262,26 @@ hifa4_status hifa4_attention_fwd(const hifa4_problem* p, const hifa4_fwd_options
                                  const float* s, void* o, float* lse,
                                  void* workspace, size_t workspace_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops, harnesses that forbid hipMalloc): hifa4_attention_fwd
+ * with its workspace in a static device array of the library,
+ * HIFA4_NOALLOC_SCRATCH_BYTES (32 MiB) per GPU, held from the first call on
+ * that GPU until the process ends.  The caller passes inputs and outputs as
+ * for hifa4_attention_fwd; the call allocates and frees nothing.  A problem
+ * whose hifa4_workspace_bytes() exceeds the array fails with
+ * HIFA4_ERR_WORKSPACE before any work is enqueued (32 MiB holds, for
+ * example, 8 kv heads of D=128 up to 10240 tokens).  The array's address on
+ * the current device (which must be the stream's device) is looked up on the
+ * first call there.  Every call on one GPU shares its array: calls that
+ * overlap on one GPU (different streams, or threads) race and give wrong
+ * results; calls ordered on one stream are safe.  Nothing in the array needs
+ * to start at zero (each call writes every entry it reads).  Otherwise
+ * identical to hifa4_attention_fwd, including the debug and timing options. */
+#define HIFA4_NOALLOC_SCRATCH_BYTES (32u << 20)
+hifa4_status hifa4_attention_fwd_noalloc(const hifa4_problem* p, const hifa4_fwd_options* opt,
+                                         const void* q, const void* k, const void* v,
+                                         const float* s, void* o, float* lse, void* stream);
+
 /* Workspace size in bytes of hifa4_decode_fwd for problem p (0 if p is
  * invalid).  It grows with batch * num_heads_q * ceil(max_seqlen/64). */
 size_t hifa4_decode_workspace_bytes(const hifa4_problem* p);

@@ -29,7 +29,8 @@ STATUS = {0: "HIFA4_OK", -1: "HIFA4_ERR_INVALID_ARGUMENT", -2: "HIFA4_ERR_UNSUPP
 EXPORTED = ("hifa4_workspace_bytes", "hifa4_calibrate_workspace_bytes", "hifa4_calibrate_smooth_qk",
             "hifa4_calibrate_smooth_qk_layers",
             "hifa4_quantize_qk", "hifa4_quantize_v", "hifa4_attention_fwd", "hifa4_decode_workspace_bytes",
-            "hifa4_decode_fwd", "hifa4_selftest_exp2", "hifa4_last_error")
+            "hifa4_decode_fwd", "hifa4_selftest_exp2", "hifa4_last_error", "hifa4_attention_fwd_noalloc")
+NOALLOC_SCRATCH_BYTES = 32 << 20
 
 
 class Problem(ctypes.Structure):
@@ -87,6 +88,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.hifa4_quantize_v.argtypes = [P(Problem), vp, vp, vp, vp]
     lib.hifa4_attention_fwd.restype = ctypes.c_int
     lib.hifa4_attention_fwd.argtypes = [P(Problem), P(FwdOptions), vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.hifa4_attention_fwd_noalloc.restype = ctypes.c_int
+    lib.hifa4_attention_fwd_noalloc.argtypes = [P(Problem), P(FwdOptions), vp, vp, vp, vp, vp, vp, vp]
     lib.hifa4_decode_workspace_bytes.restype = sz
     lib.hifa4_decode_workspace_bytes.argtypes = [P(Problem)]
     lib.hifa4_decode_fwd.restype = ctypes.c_int
@@ -314,6 +317,31 @@ def hifa4_attention_fwd(q, k, v, s=None, cu_seqlens=None, max_seqlen=None, norm:
                                    _ptr(o), _ptr(l), _ptr(ws), ws.numel(), _stream(dev)), "hifa4_attention_fwd")
     if debug_p:
         return o, l, pc, pm
+    return o, l
+
+
+def hifa4_attention_fwd_noalloc(q, k, v, s=None, cu_seqlens=None, max_seqlen=None, norm: int = NORM_PREORDER,
+                                operands: int = OPERANDS_HIF4, smooth_qk: Optional[bool] = None, out=None,
+                                lse=None):
+    """hifa4_attention_fwd with the library's static per-GPU scratch array as
+    its workspace (no device allocation inside the call; at most
+    NOALLOC_SCRATCH_BYTES of workspace).  Outputs are allocated here unless
+    `out` and `lse` are given."""
+    torch = _torch()
+    for t, n in ((q, "q"), (k, "k"), (v, "v")):
+        _require(t, torch.float16, n)
+    _require(s, torch.float32, "s")
+    sh = shape_of(q, k, cu_seqlens, max_seqlen)
+    lib = load_library()
+    dev = q.device
+    if smooth_qk is None:
+        smooth_qk = s is not None
+    o = torch.empty_like(q) if out is None else out
+    l = torch.empty((sh.heads_q, sh.tokens), dtype=torch.float32, device=dev) if lse is None else lse
+    opt = FwdOptions(norm, operands, 1 if smooth_qk else 0, None, None, None, 0)
+    p = sh.problem()
+    _check(lib.hifa4_attention_fwd_noalloc(ctypes.byref(p), ctypes.byref(opt), _ptr(q), _ptr(k), _ptr(v), _ptr(s),
+                                           _ptr(o), _ptr(l), _stream(dev)), "hifa4_attention_fwd_noalloc")
     return o, l
 
 

@@ -10,6 +10,7 @@
 #include <cstdio>
 #include <cstring>
 #include <initializer_list>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -410,3 +411,55 @@ hifa4_status hifa4_calibrate_smooth_qk_layers(const hifa4_problem* p, int32_t n_
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// hifa4_attention_fwd_noalloc: the forward with its K/V pre-pass workspace in
+// a file-scope device array (one copy per GPU, held until the process ends),
+// for callers that cannot allocate.  In host code `scratch` names a host-side
+// stand-in, never the device memory: the device address comes from
+// hipGetSymbolAddress, once per device with that device current, and only
+// that address is passed to kernels.
+static __device__ __align__(256) uint8_t scratch[HIFA4_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+hifa4_status scratch_pointer(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(HIFA4_ERR_UNSUPPORTED, "device index %d above %d", dev, kMaxDevices - 1);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!ptr) return fail(HIFA4_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return HIFA4_OK;
+}
+
+}  // namespace
+
+hifa4_status hifa4_attention_fwd_noalloc(const hifa4_problem* p, const hifa4_fwd_options* opt, const void* q,
+                                         const void* k, const void* v, const float* s, void* o, float* lse,
+                                         void* stream) {
+  Dims d;
+  hifa4_status st = check_problem(p, &d);
+  if (st != HIFA4_OK) return st;
+  if (!opt) return fail(HIFA4_ERR_INVALID_ARGUMENT, "options is NULL");
+  const size_t need = hifa4_workspace_bytes(p, opt);
+  if (need > (size_t)HIFA4_NOALLOC_SCRATCH_BYTES)
+    return fail(HIFA4_ERR_WORKSPACE,
+                "problem needs %zu bytes of scratch; hifa4_attention_fwd_noalloc holds at most %zu "
+                "(use hifa4_attention_fwd with a caller workspace)",
+                need, (size_t)HIFA4_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  if ((st = scratch_pointer(&ws)) != HIFA4_OK) return st;
+  return hifa4_attention_fwd(p, opt, q, k, v, s, o, lse, ws, (size_t)HIFA4_NOALLOC_SCRATCH_BYTES, stream);
+}

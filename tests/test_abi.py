@@ -71,6 +71,20 @@ def test_validation_codes(lib):
     assert lib.hifa4_selftest_exp2(None, None, -1, None) == -1
 
 
+def test_noalloc_refuses_oversized_before_any_work(lib):
+    """The no-allocation entry point checks the workspace a problem needs
+    against its static array before it touches the GPU (this runs without
+    one)."""
+    p = _p(max_seqlen=16384, num_heads_q=32, num_heads_kv=8)
+    opt = h.FwdOptions(0, 0, 0, None, None, None)
+    assert lib.hifa4_workspace_bytes(ctypes.byref(p), ctypes.byref(opt)) > h.NOALLOC_SCRATCH_BYTES
+    assert lib.hifa4_attention_fwd_noalloc(ctypes.byref(p), ctypes.byref(opt), FAKE, FAKE, FAKE, None, FAKE,
+                                           FAKE, None) == -3
+    assert "at most" in h.hifa4_last_error()
+    assert lib.hifa4_attention_fwd_noalloc(ctypes.byref(_p(head_dim=96)), ctypes.byref(opt), FAKE, FAKE, FAKE,
+                                           None, FAKE, FAKE, None) == -2
+
+
 def test_workspace_sizes(lib):
     p = _p(max_seqlen=4096, num_heads_q=32, num_heads_kv=8)
     o = h.FwdOptions(0, 0, 0, None, None, None)
