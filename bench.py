@@ -562,6 +562,8 @@ def main():
     ap.add_argument("--no-decode", action="store_true", help="skip the decode step over the packed cache")
     ap.add_argument("--decode-only", action="store_true",
                     help="only time the decode step (for profiling its kernels) and print its report")
+    ap.add_argument("--issue-probe", action="store_true",
+                    help="only run the instruction issue-cost probe (built with the library) and print its lines")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB five times (the reference kernel that "
                          "scales HBM traffic counters) and exit")
@@ -572,6 +574,13 @@ def main():
               "cross-GPU exchange, and this build measures one GPU's share.  Use --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
+    if args.issue_probe:
+        import subprocess
+        probe = os.path.join(ROOT, "paper_2607_04302_amd", "issue_probe")
+        if not os.path.exists(probe):
+            print("issue_probe not built (python -m paper_2607_04302_amd.build)", file=sys.stderr)
+            sys.exit(1)
+        sys.exit(subprocess.run([probe]).returncode)
     import numpy as np
     import torch
     if args.copy_probe:

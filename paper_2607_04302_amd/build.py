@@ -55,6 +55,12 @@ def build(verbose: bool = False) -> str:
     tmp = LIB + ".tmp"
     subprocess.check_call([hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp])
     os.replace(tmp, LIB)
+    # the instruction issue-cost probe behind bench.py --issue-probe (not part of the library)
+    probe = os.path.join(HERE, "issue_probe")
+    subprocess.check_call([hipcc(), "--offload-arch=gfx950", "-O3", "-Xclang", "-target-feature", "-Xclang",
+                           "-packed-fp32-ops", os.path.join(CSRC, "issue_probe.hip"), "-o", probe + ".tmp"],
+                          stderr=subprocess.DEVNULL)
+    os.replace(probe + ".tmp", probe)
     return LIB
 
 
