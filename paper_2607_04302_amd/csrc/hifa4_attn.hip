@@ -115,6 +115,15 @@ __device__ __forceinline__ void stage_chunk_async(uint8_t* lds, const uint8_t* _
 
 __device__ __forceinline__ void wait_async_copies() { __builtin_amdgcn_s_waitcnt(0x0F70); }   // vmcnt(0)
 
+// vmcnt(N): at most N vector-memory operations of the wave outstanding (they
+// complete in issue order).  gfx9 encoding: vmcnt low bits [3:0], high bits
+// [15:14]; expcnt and lgkmcnt left at their maxima.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_k() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x0F70);
+}
+
 // One lane's 24-byte FP6 operand from an operand record (64 lanes x 16
 // bytes, then 64 lanes x 8 bytes).  The 8-byte tail is read through a volatile
 // access so that the compiler does not pair it with the tail of another
@@ -602,12 +611,21 @@ __global__ void __launch_bounds__(256, (G == 1 ? 4 : (G == 2 ? 3 : 1))) k_attn_h
 // halves of S^T and the D/32 channel tiles of O^T are independent MFMA
 // chains, issued interleaved.
 template <int D>
-__global__ void __launch_bounds__(256, (D <= 128 ? 2 : 1)) k_attn_fp16(AttnArgs a, int heads_per_wg, int qsub, int n_qtiles) {
+__global__ void __launch_bounds__(256, (D <= 128 ? 3 : 1)) k_attn_fp16(AttnArgs a, int heads_per_wg, int qsub, int n_qtiles) {
   constexpr int KC = D / 16;
   constexpr int DT = D / 32;
   constexpr ChunkLayout lay = chunk_layout_fp16(D);
   constexpr int cbytes = (int)lay.bytes;
+  constexpr int KB = (int)lay.v_op;               // K operands of a chunk (first part)
+  constexpr int VB = cbytes - KB;                 // V operands (second part)
+  // whole pieces only, so every wave issues the same number of K pieces and
+  // vmcnt(K pieces) leaves only those outstanding
+  static_assert(KB % 4096 == 0 && VB % 4096 == 0, "fp16 chunk parts must be whole 4 KiB pieces");
   extern __shared__ __align__(16) uint8_t smem[];
+  // K of blocks J and J+1 in two buffers, V of block J in one: V streams in
+  // at the start of its block and is waited for just before the PV MFMAs
+  uint8_t* kbuf = smem;
+  uint8_t* vbuf = smem + 2 * KB;
   const TileMap tm = map_tile(a, heads_per_wg, qsub, n_qtiles);
   if (!tm.wg_live) return;
   const int lane = threadIdx.x & 63, h = lane >> 5, col = lane & 31;
@@ -625,7 +643,7 @@ __global__ void __launch_bounds__(256, (D <= 128 ? 2 : 1)) k_attn_fp16(AttnArgs 
     else
       for (int e = 0; e < 8; ++e) qf[kc][e] = (half_t)0.0f;
   }
-  stage_chunk_async<cbytes>(smem, ws_base);
+  stream_pieces_from<KB>(ChunkStream{kbuf, ws_base, wave_u}, 0);
   f16v_t O[DT];
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt)
@@ -638,20 +656,23 @@ __global__ void __launch_bounds__(256, (D <= 128 ? 2 : 1)) k_attn_fp16(AttnArgs 
 
   for (int J = 0; J < tm.nJ; ++J) {
     set_priority_by_work_left(tm.nJ - J);
-    const uint8_t* cur = smem + (J & 1) * cbytes;
-    const ChunkStream cs{smem + ((J + 1) & 1) * cbytes, ws_base + (size_t)(J + 1 < tm.nJ ? J + 1 : J) * cbytes,
-                         wave_u};
+    const uint8_t* kc_cur = kbuf + (J & 1) * KB;
+    const uint8_t* chunkJ = ws_base + (size_t)J * cbytes;
+    // V of this block now (its buffer is free since the last block's PV);
+    // K of the next block into the other K buffer during the block
+    stream_pieces_from<VB>(ChunkStream{vbuf, chunkJ + KB, wave_u}, 0);
+    const ChunkStream cs{kbuf + ((J + 1) & 1) * KB, ws_base + (size_t)(J + 1 < tm.nJ ? J + 1 : J) * cbytes, wave_u};
+    constexpr int kKPieces = (KB / 16 + 255) / 256;
     if (tm.active && J <= jw_last) {
-      stream_piece<cbytes>(cs, 0);
       f16v_t acc[2] = {};
 #pragma unroll
       for (int kc = 0; kc < KC; ++kc)
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
-          const h8_t kf = *reinterpret_cast<const h8_t*>(cur + lay.k_op + ((size_t)(t * KC + kc) * 64 + lane) * 16);
+          const h8_t kf = *reinterpret_cast<const h8_t*>(kc_cur + ((size_t)(t * KC + kc) * 64 + lane) * 16);
           acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf, qf[kc], acc[t], 0, 0, 0);
         }
-      stream_piece<cbytes>(cs, 1);
+      stream_piece<KB>(cs, 0);
       h2_t s2[2][8];
 #pragma unroll
       for (int t = 0; t < 2; ++t)
@@ -669,7 +690,7 @@ __global__ void __launch_bounds__(256, (D <= 128 ? 2 : 1)) k_attn_fp16(AttnArgs 
       mx2 = hmax_halves(max_with_partner(mx2));
       const h2_t mr2 = {m_run, m_run};
       const h2_t mn2 = hmax2(mr2, mx2);
-      stream_piece<cbytes>(cs, 2);
+      stream_piece<KB>(cs, 1);
       h2_t p2[2][8];
 #pragma unroll
       for (int t = 0; t < 2; ++t)
@@ -690,7 +711,7 @@ __global__ void __launch_bounds__(256, (D <= 128 ? 2 : 1)) k_attn_fp16(AttnArgs 
       const float r = (float)rr[0];
       m_run = mn2[0];
       l_sum = l_sum * r + ps;
-      stream_piece<cbytes>(cs, 3);
+      stream_pieces_from<KB>(cs, 2);
       if (__builtin_amdgcn_ballot_w64(r != 1.0f) != 0) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
@@ -709,18 +730,24 @@ __global__ void __launch_bounds__(256, (D <= 128 ? 2 : 1)) k_attn_fp16(AttnArgs 
           pb[c][2 * e + 1] = p2[t][4 * jp + e][1];
         }
       }
+      // V of this block: the wave's own pieces (issued before its K pieces)
+      // have landed once at most the K pieces are outstanding; then every
+      // wave's share is visible after the barrier
+      wait_vmcnt_k<kKPieces>();
+      __syncthreads();
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
-          const h8_t vf = *reinterpret_cast<const h8_t*>(cur + lay.v_op + ((size_t)(dt * 4 + c) * 64 + lane) * 16);
+          const h8_t vf = *reinterpret_cast<const h8_t*>(vbuf + ((size_t)(dt * 4 + c) * 64 + lane) * 16);
           O[dt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pb[c], O[dt], 0, 0, 0);
         }
-        stream_piece<cbytes>(cs, 4 + c);
       }
-      stream_pieces_from<cbytes>(cs, 8);
     } else {
-      stream_pieces_from<cbytes>(cs, 0);
+      stream_pieces_from<KB>(cs, 0);
+      // the barrier the computing waves take before their PV MFMAs
+      wait_vmcnt_k<kKPieces>();
+      __syncthreads();
     }
     wait_async_copies();
     __syncthreads();
@@ -965,7 +992,7 @@ hipError_t launch_attention(const AttnArgs& a, int norm, int operands, bool qmea
     return hipErrorInvalidValue;
   }
   if (operands == 1) {
-    const size_t lds = 2 * chunk_layout_fp16(a.D).bytes;
+    const size_t lds = 2 * chunk_layout_fp16(a.D).v_op + (chunk_layout_fp16(a.D).bytes - chunk_layout_fp16(a.D).v_op);
     switch (a.D) {
       case 64: return launch_k(k_attn_fp16<64>, a, lds, st);
       case 128: return launch_k(k_attn_fp16<128>, a, lds, st);
