@@ -567,6 +567,9 @@ def main():
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the throughput of the other workloads (tiny, long, varlen, wide)")
     ap.add_argument("--no-decode", action="store_true", help="skip the decode step over the packed cache")
+    ap.add_argument("--no-clock-query", action="store_true",
+                    help="skip the rocm-smi clock reading (a child process); for runs under a profiler, whose "
+                         "preloaded library has initialised the GPU in the process the child is forked from")
     ap.add_argument("--decode-only", action="store_true",
                     help="only time the decode step (for profiling its kernels) and print its report")
     ap.add_argument("--issue-probe", action="store_true",
@@ -671,7 +674,7 @@ def main():
         "clock_settle_calls": settle,
         "valu_roofline": valu_roofline(read_sq(f"attn_hif4_{w.name}_sq_counters.txt"), att_ms),
         "call_device_time": call_distribution(h, torch, np, q, k, v, s, ws),
-        "sclk_mhz_during_calls": observed_sclk(h, torch, q, k, v, s, ws),
+        "sclk_mhz_during_calls": None if args.no_clock_query else observed_sclk(h, torch, q, k, v, s, ws),
     }
     if not args.no_variants:
         wall16, pre16, att16, out16, _ = time_variant(h, torch, args, q, k, v, None, h.NORM_PREORDER,
