@@ -57,6 +57,25 @@ VALU_KERNEL(k_exp_f32, "v_exp_f32 %0, %0")
 VALU_KERNEL(k_rcp_f32, "v_rcp_f32 %0, %0")
 VALU_KERNEL(k_permlane32_swap, "v_permlane32_swap_b32 %0, %1")
 
+// 64-bit address arithmetic (the form the compiler emits for global
+// addresses built from a per-lane base and a uniform offset)
+__global__ void __launch_bounds__(256) k_lshl_add_u64(const unsigned* in, unsigned* out, int iters) {
+  unsigned long long a[kChains];
+  const unsigned long long b =
+      ((unsigned long long)in[threadIdx.x & 63] << 32) | (unsigned long long)in[64 + (threadIdx.x & 63)];
+  for (int i = 0; i < kChains; ++i) a[i] = in[128 + i] ^ threadIdx.x;
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int r = 0; r < kRounds; ++r) {
+#pragma unroll
+      for (int i = 0; i < kChains; ++i) asm volatile("v_lshl_add_u64 %0, %0, 0, %1" : "+v"(a[i]) : "v"(b));
+    }
+  }
+  unsigned s = 0;
+  for (int i = 0; i < kChains; ++i) s ^= (unsigned)a[i] ^ (unsigned)(a[i] >> 32);
+  out[blockIdx.x * blockDim.x + threadIdx.x] = s;
+}
+
 constexpr int kMfmaChains = 4;
 __global__ void __launch_bounds__(256) k_mfma_fp6(const unsigned* in, unsigned* out, int iters) {
   i8v a, b;
@@ -139,6 +158,7 @@ int main() {
       {"v_cmp_gt_u32+v_cndmask_b32", k_cmp_cndmask, 400, v}, {"v_fma_mix_f32", k_fma_mix_f32, 400, v},
       {"v_fma_mixlo_f16", k_fma_mixlo_f16, 400, v}, {"v_exp_f16", k_exp_f16, 400, v}, {"v_exp_f32", k_exp_f32, 400, v},
       {"v_rcp_f32", k_rcp_f32, 400, v}, {"v_permlane32_swap_b32", k_permlane32_swap, 400, v},
+      {"v_lshl_add_u64", k_lshl_add_u64, 400, v},
       {"v_mfma_scale_f32_32x32x64_f8f6f4 (fp6)", k_mfma_fp6, 200, kMfmaChains},
       {"v_mfma_f32_32x32x16_f16", k_mfma_f16, 200, kMfmaChains},
       {"v_cvt_scalef32_pk32_fp6_f16", k_cvt_pk32_fp6_f16, 200, 8}};
