@@ -75,15 +75,29 @@ __device__ __forceinline__ void stage_chunk(uint8_t* lds, const uint8_t* __restr
   for (int i = threadIdx.x; i < bytes / 16; i += blockDim.x) dst[i] = src[i];
 }
 
+// A wave-uniform pointer read into scalar registers (its value is the same in
+// every lane; the compiler cannot see that for values derived from the wave
+// index).
+__device__ __forceinline__ const uint8_t* uniform_ptr(const uint8_t* p) {
+  const uint64_t u = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
+  return reinterpret_cast<const uint8_t*>(((uint64_t)hi << 32) | lo);
+}
+
 // Asynchronous copy of one chunk (BYTES, a multiple of 1 KiB) from global
 // memory straight into LDS (global_load_lds, 16 bytes per lane; lane i of a
 // wave lands at the wave's LDS base + 16 i), in pieces of 256 lanes x 16
 // bytes.  On the last block of a tile the current chunk is streamed into the
 // idle buffer again, which keeps the block code free of branches.
 // Completion is tracked by vmcnt: the caller waits with vmcnt(0) and a
-// barrier before reading.  Issuing a piece stalls the wave while the
-// texture path is busy, so the block code spreads the pieces over its phases
-// instead of issuing the whole chunk at once.
+// barrier before reading.  Issuing a piece stalls the wave while the texture
+// path is busy, so the block code spreads the pieces over its phases instead
+// of issuing the whole chunk at once.  The load is written out (M0 set to the
+// wave's LDS destination, the global base in scalar registers, the lane's
+// 16-byte offset in one VGPR) because the compiler forms the address of the
+// builtin form with 64-bit vector adds per piece; the hardware counts these
+// loads in vmcnt like any other and completes them in issue order.
 struct ChunkStream {
   uint8_t* dst;            // LDS buffer
   const uint8_t* src;      // global chunk (the last block streams a copy of itself)
@@ -97,9 +111,16 @@ __device__ __forceinline__ void stream_piece(const ChunkStream& cs, int r) {
   // every piece but possibly the last covers all four waves (n16 is a
   // multiple of 64); the conditions are uniform, so no lane masking
   if (256 * (r + 1) > n16 && 256 * r + 64 * cs.wave >= n16) return;
-  __builtin_amdgcn_global_load_lds(
-      (const __attribute__((address_space(1))) void*)(cs.src + 4096 * r + 1024 * cs.wave + 16 * (threadIdx.x & 63)),
-      (__attribute__((address_space(3))) void*)(cs.dst + 4096 * r + 1024 * cs.wave), 16, 0, 0);
+  // global_load_lds_dwordx4 with a scalar base: lane i reads 16 bytes at
+  // base + 16 i and writes them to LDS at M0 + 16 i
+  const uint8_t* gbase = cs.src + (4096 * r + 1024 * cs.wave);
+  uint8_t* const ldst = cs.dst + 4096 * r + 1024 * cs.wave;
+  const uint32_t m0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)ldst;
+  const uint32_t voff = 16u * (threadIdx.x & 63u);
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(gbase), "s"(m0)
+               : "memory", "m0");
 }
 
 template <int BYTES>
@@ -518,7 +539,7 @@ __global__ void __launch_bounds__(256, (G == 1 ? 4 : (G == 2 ? 3 : 1))) k_attn_h
   const bool row_ok = tm.active && qi < tm.L;
   const int jw_last = tm.active ? (min(tm.qw + 31, tm.L - 1)) / 64 : -1;
   // the first K/V chunk streams into LDS while the Q tile is quantized
-  const uint8_t* ws_base = a.ws + ((size_t)(tm.b * a.hkv + tm.hk) * a.NB) * lay.bytes;
+  const uint8_t* ws_base = uniform_ptr(a.ws + ((size_t)(tm.b * a.hkv + tm.hk) * a.NB) * lay.bytes);
   const int wave_u = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   // ---- Q tile: Smooth-QK (fp16(q*s)) then HIF4 into FP6 B operands.  The
   // Q rows and scales are requested before the chunk stream, whose
@@ -632,7 +653,7 @@ __global__ void __launch_bounds__(256, (D <= 128 ? 3 : 1)) k_attn_fp16(AttnArgs 
   const int qi = tm.qw + col;
   const bool row_ok = tm.active && qi < tm.L;
   const int jw_last = tm.active ? (min(tm.qw + 31, tm.L - 1)) / 64 : -1;
-  const uint8_t* ws_base = a.ws + ((size_t)(tm.b * a.hkv + tm.hk) * a.NB) * lay.bytes;
+  const uint8_t* ws_base = uniform_ptr(a.ws + ((size_t)(tm.b * a.hkv + tm.hk) * a.NB) * lay.bytes);
   const int wave_u = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
 
   h8_t qf[KC];
@@ -791,7 +812,7 @@ __global__ void __launch_bounds__(256, (D <= 128 ? 2 : 1)) k_attn_ponly(AttnArgs
   const int qi = tm.qw + col;
   const bool row_ok = tm.active && qi < tm.L;
   const int jw_last = tm.active ? (min(tm.qw + 31, tm.L - 1)) / 64 : -1;
-  const uint8_t* ws_base = a.ws + ((size_t)(tm.b * a.hkv + tm.hk) * a.NB) * lay.bytes;
+  const uint8_t* ws_base = uniform_ptr(a.ws + ((size_t)(tm.b * a.hkv + tm.hk) * a.NB) * lay.bytes);
   const int wave_u = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
 
   h8_t qf[KC];
