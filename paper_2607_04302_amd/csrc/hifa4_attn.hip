@@ -97,7 +97,10 @@ __device__ __forceinline__ const uint8_t* uniform_ptr(const uint8_t* p) {
 // wave's LDS destination, the global base in scalar registers, the lane's
 // 16-byte offset in one VGPR) because the compiler forms the address of the
 // builtin form with 64-bit vector adds per piece; the hardware counts these
-// loads in vmcnt like any other and completes them in issue order.
+// loads in vmcnt like any other and completes them in issue order.  The
+// compiler treats M0 as reserved and keeps no value of its own there across
+// the statement, so nothing else in this file may use M0
+// (tests/test_m0_guard.py checks the compiled code).
 struct ChunkStream {
   uint8_t* dst;            // LDS buffer
   const uint8_t* src;      // global chunk (the last block streams a copy of itself)
